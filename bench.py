@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Throughput of the PGC step on one MI355X.
+
+One "step" is one pipelined PGC step (t >= 1) of the whole hot path: the
+per-partition gradients of every evaluated partition, the ring write, the
+encode of every worker's coded gradient, the masked decode and the update,
+over the full synthetic dataset resident in HBM.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints one JSON line.  `value` is steps/s; `roofline` is the gradient kernel
+(the dominant one) against the 8 TB/s HBM peak, timed with HIP events around
+each of its launches inside the timed region; `cpu_baseline` is the fp64
+oracle on the host cores over a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "crreal_lsq_n8_c3_d1024"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def rows_per_step(w):
+    """Rows the pipelined step streams: all N for CR, one partition per FR group."""
+    return w.N // w.c if w.scheme == "FR" else w.N
+
+
+def algorithmic_bytes(w):
+    """(gradient-kernel bytes per launch, whole-step bytes) of a pipelined step.
+
+    Gradient kernel: each evaluated row once (4d bytes of features + 4 of label)
+    plus w.  Whole step adds the fresh-gradient writes, one read of every ring
+    slot the encode combines, the coded-gradient writes, the decoded vector and
+    the update's read and write of w.
+    """
+    q = w.q
+    rows = rows_per_step(w)
+    n_eval = w.n // w.c if w.scheme == "FR" else w.n
+    planes_read = w.n if w.scheme == "FR" else w.n * w.c
+    n_coded = w.n // w.c if w.scheme == "FR" else w.n
+    grad = rows * (4 * w.d + 4) + 4 * q
+    step = grad + 4 * q * (n_eval + planes_read + n_coded + 1 + 2)
+    return grad, step
+
+
+def read_traffic(workload):
+    """HBM bytes per gradient launch measured by rocprofv3 counters, if they were
+    taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = data.get(workload)
+    if not entry or entry.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(w, X, y, beta0, budget_s):
+    """The oracle, as it stands, on the host over the first steps of the same run."""
+    from threadpoolctl import threadpool_info
+    from oracle import pgc_oracle as O
+    from oracle import rng as R
+    schemes = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
+    B = None
+    if w.scheme == "CR_REAL":
+        B = O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
+    max_steps = 100000
+    Xh, yh, bh = X.cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy()
+
+    def run(steps):
+        masks = [R.straggler_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(steps)]
+        t0 = time.perf_counter()
+        O.run(schemes[w.scheme], w.model, w.n, w.c, Xh, yh, bh, w.lr, masks, B=B,
+              keep_coded=False, keep_alpha=False)
+        return time.perf_counter() - t0
+
+    t2, t6 = run(2), run(6)
+    per_step = max((t6 - t2) / 4, 1e-6)
+    fixed = max(t2 - 2 * per_step, 0.0)
+    steps = int(max(2, min(max_steps, (budget_s - fixed) / per_step)))
+    elapsed = run(steps)
+    threads = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+    cores = min(max(threads) if threads else 1, len(os.sched_getaffinity(0)))
+    return {"value": steps / elapsed, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": "fp64 numpy oracle over steps t=0..%d of the same workload and masks "
+                      "(%.1f s wall, including its one-time fp64 copy of X)" % (steps - 1, elapsed)}
+
+
+def copy_calibration(nbytes):
+    """Launch torch's copy kernel on nbytes bytes 20 times: it reads and writes
+    exactly nbytes per launch, which scales the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(20):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("copied %d bytes 20 times" % (src.numel() * 4))
+    return 0
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="wall-time budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes 20 times and exit "
+                         "(a known-size reference for the HBM byte counters)")
+    args = ap.parse_args()
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        return 2
+    if args.steps < 1 or args.warmup < 1:
+        print("--steps and --warmup must be >= 1 (the first warm-up step is the pipeline fill t = 0)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2607_20739_amd as P
+    from workloads import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log("workload %s: generating inputs" % w.name)
+    X, y, beta0 = make_inputs(w, device=dev)
+    total = args.warmup + args.steps
+    masks = [P.pgc_make_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(total)]
+    sess = P.PGCSession(w.scheme, w.n, w.c, w.model, w.N, w.d, hidden=w.hidden, classes=w.classes,
+                        code_seed=w.code_seed, device=dev)
+    wv = beta0.clone()
+    log("warm-up: %d steps (t = 0 fills the pipeline)" % args.warmup)
+    for t in range(args.warmup):
+        sess.step(X, y, wv, masks[t], w.lr)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    P.pgc_set_timing(sess.ctx, True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for t in range(args.warmup, total):
+        sess.step(X, y, wv, masks[t], w.lr)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    elapsed_ms = start.elapsed_time(stop)
+    grad_ms, grad_launches = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_GRADIENT)
+    red_ms, _ = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_REDUCE)
+    code_ms, _ = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_CODE)
+    P.pgc_set_timing(sess.ctx, False)
+    if not bool(torch.isfinite(wv).all()):
+        print("non-finite weights after the timed steps", file=sys.stderr)
+        return 1
+
+    ms_per_step = elapsed_ms / args.steps
+    steps_per_s = 1000.0 / ms_per_step
+    grad_bytes, step_bytes = algorithmic_bytes(w)
+    grad_avg_ms = grad_ms / grad_launches
+    achieved = grad_bytes / (grad_avg_ms * 1e-3) / 1e9
+    traffic = read_traffic(w.name)
+    log("step %.4f ms; gradient %.4f ms, reduce %.4f ms, code %.4f ms per launch"
+        % (ms_per_step, grad_avg_ms, red_ms / args.steps, code_ms / args.steps))
+
+    baseline = None
+    if args.cpu_seconds > 0:
+        log("oracle baseline on the host (budget %.0f s)" % args.cpu_seconds)
+        baseline = cpu_baseline(w, X, y, beta0, args.cpu_seconds)
+
+    rows = rows_per_step(w)
+    out = {
+        "metric": "PGC steps/sec & samples/sec at 1 MI355X; achieved HBM GB/s vs peak",
+        "value": steps_per_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "scheme": w.scheme, "loss": w.model, "n": w.n, "c": w.c,
+                   "N": w.N, "d": w.d, "lr": w.lr},
+        "samples_per_s": {"unique_rows": rows * steps_per_s, "worker_samples": w.N * steps_per_s},
+        "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
+        "kernel_ms_per_step": {"gradient": grad_avg_ms, "reduce": red_ms / args.steps,
+                               "code": code_ms / args.steps},
+        "roofline": {"bound": "hbm", "kernel": "linear_gradient_kernel", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "cpu_baseline": baseline,
+    }
+    print(json.dumps(out), flush=True)
+    sess.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,163 @@
+"""The C-ABI library on the host (no GPU): exports, host tables, error codes.
+
+Host tables are compared with the oracle: placement, schedule, straggler masks
+and surviving sets bit for bit; the real-valued code's matrix and decode
+weights within 1e-12.  No device work is launched here.
+"""
+
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_20739_amd as P
+from oracle import pgc_oracle as O
+from oracle import rng as R
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SCHEME_NAMES = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
+
+
+def _declared_symbols():
+    with open(os.path.join(ROOT, "include", "pgc.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(pgc_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared_symbols()
+    assert len(declared) >= 20
+    assert declared == sorted(P.exported_symbols())
+    handle = P.lib()
+    for name in declared:
+        assert hasattr(handle, name), name
+
+
+def _ctx(scheme, n, c, d=8, model="lsq", N=None, code_seed=0):
+    ctx = P.pgc_init(scheme, n, c, d)
+    P.pgc_configure(ctx, model, N if N is not None else n * 4, d, code_seed=code_seed)
+    return ctx
+
+
+CASES = [("FR", 4, 2), ("FR", 32, 4), ("FR", 6, 6), ("FR", 5, 1), ("CR", 8, 3), ("CR", 64, 4),
+         ("CR", 128, 8), ("CR", 7, 7), ("CR_REAL", 8, 3), ("CR_REAL", 12, 6), ("CR_REAL", 4, 2),
+         ("CR_REAL", 5, 1)]
+
+
+@pytest.mark.parametrize("scheme,n,c", CASES)
+def test_placement_and_schedule_match_the_oracle(scheme, n, c):
+    ctx = _ctx(scheme, n, c)
+    try:
+        P_or = O.placement(SCHEME_NAMES[scheme], n, c)
+        assert P.pgc_placement(ctx, n, c).tolist() == P_or
+        for t in range(1, 3 * c + 2):
+            expect = [P_or[i][O.evaluated_slot(t, c)] for i in range(n)]
+            assert P.pgc_schedule(ctx, t, n).tolist() == expect
+        assert P.pgc_num_coded(ctx) == (n // c if scheme == "FR" else n)
+        with pytest.raises(P.PGCError):
+            P.pgc_schedule(ctx, 0, n)
+    finally:
+        P.pgc_destroy(ctx)
+
+
+def test_splitmix64_matches_the_oracle():
+    for seed in [0, 1, 1234567, (5 << 32) | 1, 2 ** 64 - 1]:
+        for index in [0, 1, 2, 77, 2 ** 32 + 3, 2 ** 40]:
+            assert P.pgc_splitmix64(seed, index) == R.splitmix64(seed, index)
+
+
+@pytest.mark.parametrize("policy,n,cap,p", [
+    (R.POLICY_EXACT, 4, 1, 0.0), (R.POLICY_UNIFORM_COUNT, 8, 2, 0.0), (R.POLICY_BERNOULLI, 32, 3, 0.05),
+    (R.POLICY_BERNOULLI, 64, 3, 0.05), (R.POLICY_BERNOULLI, 128, 7, 0.04), (R.POLICY_BERNOULLI, 16, 2, 0.5),
+    (R.POLICY_EXACT, 256, 255, 0.0), (R.POLICY_UNIFORM_COUNT, 1, 0, 0.0)])
+def test_masks_match_the_oracle_bit_for_bit(policy, n, cap, p):
+    for seed in [(1 << 32) | 1, (5 << 32) | 1, 99]:
+        for t in range(60):
+            a = P.pgc_make_mask(seed, t, policy, n, cap, p)
+            b = R.straggler_mask(seed, t, policy, n, cap, p)
+            assert a.tolist() == b.tolist(), (seed, t)
+
+
+@pytest.mark.parametrize("n,c,seed", [(4, 2, 1), (8, 3, 2), (12, 6, 3), (5, 1, 4), (16, 5, 9)])
+def test_real_code_matrix_matches_the_oracle(n, c, seed):
+    ctx = _ctx("CR_REAL", n, c, code_seed=seed)
+    try:
+        B = P.pgc_encoding_matrix(ctx, n)
+        H = R.null_space_generator(seed, c - 1, n)
+        B_or = O.cyclic_encoding_matrix(n, c, H)
+        np.testing.assert_allclose(B, B_or, rtol=1e-12, atol=1e-12)
+        assert np.array_equal(B != 0.0, B_or != 0.0)
+    finally:
+        P.pgc_destroy(ctx)
+
+
+@pytest.mark.parametrize("scheme,n,c", [("FR", 6, 3), ("FR", 8, 2), ("CR", 7, 3), ("CR_REAL", 8, 3),
+                                        ("CR_REAL", 6, 4), ("CR_REAL", 12, 6)])
+def test_decode_coefficients_match_the_oracle_for_every_admissible_mask(scheme, n, c):
+    ctx = _ctx(scheme, n, c, code_seed=5)
+    try:
+        B = P.pgc_encoding_matrix(ctx, n) if scheme == "CR_REAL" else None
+        B_or = O.cyclic_encoding_matrix(n, c, R.null_space_generator(5, c - 1, n)) if B is not None else None
+        for k in range(c):
+            for strag in itertools.combinations(range(n), k):
+                mask = np.zeros(n, np.uint8)
+                mask[list(strag)] = 1
+                surv, d, scale = P.pgc_decode_coeffs(ctx, mask, n)
+                J = O.survivors(mask)
+                d_or, scale_or = O.decode_weights(SCHEME_NAMES[scheme], n, c, J, B_or)
+                assert surv.tolist() == J
+                assert scale == pytest.approx(scale_or, rel=1e-15)
+                np.testing.assert_allclose(d, d_or, rtol=1e-10, atol=1e-10 * max(1.0, np.abs(d_or).max()))
+                if scheme != "CR_REAL":
+                    assert d.tolist() == d_or.tolist()
+    finally:
+        P.pgc_destroy(ctx)
+
+
+def test_error_codes():
+    with pytest.raises(P.PGCError) as e:
+        P.pgc_init("FR", 6, 4, 8)                      # c does not divide n
+    assert e.value.status == P.PGC_EINVAL
+    for args in [("CR", 0, 1, 8), ("CR", 4, 5, 8), ("CR", 300, 2, 8), ("CR", 4, 2, 0), (7, 4, 2, 8)]:
+        with pytest.raises(P.PGCError):
+            P.pgc_init(*args)
+    ctx = P.pgc_init("CR", 8, 3, 16)
+    try:
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_workspace_bytes(ctx)                 # not configured
+        assert e.value.status == P.PGC_ESTATE
+        for bad in [dict(model="lsq", N=12, d_in=16), dict(model="lsq", N=0, d_in=16),
+                    dict(model="lsq", N=16, d_in=15), dict(model=9, N=16, d_in=16)]:
+            with pytest.raises(P.PGCError) as e:
+                P.pgc_configure(ctx, **bad)
+            assert e.value.status == P.PGC_EINVAL
+        P.pgc_configure(ctx, "lsq", 64, 16)
+        mask = np.zeros(8, np.uint8)
+        mask[:3] = 1                                    # three stragglers > s = 2
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_decode_coeffs(ctx, mask, 8)
+        assert e.value.status == P.PGC_ESTRAGGLERS
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_step(ctx, 1, 1, 1, np.zeros(8, np.uint8), 0.1, 8)   # no workspace bound
+        assert e.value.status == P.PGC_ESTATE
+        assert P.pgc_get_step(ctx) == 0
+        assert "workspace" in P.pgc_last_error(ctx)
+    finally:
+        P.pgc_destroy(ctx)
+    assert P.pgc_strerror(P.PGC_ESTRAGGLERS)
+
+
+def test_workspace_size_covers_ring_coded_and_partials():
+    for scheme, n, c, d, N in [("FR", 4, 2, 64, 4096), ("CR_REAL", 8, 3, 1024, 262144),
+                               ("FR", 32, 4, 4096, 1048576), ("CR", 128, 8, 8192, 2097152)]:
+        ctx = _ctx(scheme, n, c, d=d, N=N, model="logistic" if scheme != "CR_REAL" else "lsq")
+        try:
+            planes = 1 if scheme == "FR" else c
+            coded = n // c if scheme == "FR" else n
+            need = 4 * d * (planes * n + coded + 1)
+            assert P.pgc_workspace_bytes(ctx) >= need
+            assert P.pgc_workspace_bytes(ctx) % 256 == 0
+        finally:
+            P.pgc_destroy(ctx)

@@ -1,0 +1,231 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Every case feeds both sides the same seeded inputs.  Straggler masks come
+from each side's own generator and must agree bit for bit; then the decoded
+gradient and the weights are compared after every step of independent
+trajectories (no re-syncing), normwise within 1e-5.
+
+Sizes: the small workloads run whole; the two large ones run their full
+trajectories with fewer rows per partition (same n, c, d, kernel shape) and,
+at full size, are checked on sampled partitions and by properties that hold
+at any size.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_20739_amd as P
+from oracle import pgc_oracle as O
+from workloads import WORKLOADS, Workload, make_inputs, POLICY_BERNOULLI, POLICY_EXACT, \
+    POLICY_UNIFORM_COUNT
+
+from _parity import FP32_TOL, gpu_masks, gpu_run, gpu_session, normwise_error, oracle_masks, \
+    oracle_run
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(what):
+    print("\n[gpu case] " + what, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    P.lib()  # fails loudly when the library is not built
+
+
+def _to_host(*tensors):
+    return [t.cpu().numpy() for t in tensors]
+
+
+def _check_trajectory(w, X, y, beta0, steps=None, X_host=None):
+    masks_gpu = gpu_masks(w, steps)
+    masks_or = oracle_masks(w, steps)
+    for t, (a, b) in enumerate(zip(masks_gpu, masks_or)):
+        assert a.tolist() == b.tolist(), "mask of step %d differs" % t
+    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu)
+    Xh = X_host if X_host is not None else X.cpu().numpy()
+    yh, bh = _to_host(y, beta0)
+    recs_or = oracle_run(w, Xh, yh, bh, masks_or)
+    worst = 0.0
+    for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
+        e_g = normwise_error(g["ghat"], o.ghat)
+        e_w = normwise_error(g["w"], o.beta)
+        worst = max(worst, e_g, e_w)
+        assert e_g <= FP32_TOL, "step %d: decoded gradient error %.3g" % (t, e_g)
+        assert e_w <= FP32_TOL, "step %d: weight error %.3g" % (t, e_w)
+    print("  worst normwise error over %d steps: %.3g" % (len(recs_gpu), worst), flush=True)
+    return recs_or
+
+
+# --------------------------------------------------------------------------
+# Whole trajectories
+# --------------------------------------------------------------------------
+
+TRAJECTORIES = [
+    ("fr_logistic_n4_c2_d64", {}),
+    ("crreal_lsq_n8_c3_d1024", {}),
+    ("fr_logistic_n32_c4_d4096", dict(N=32 * 512)),
+    ("cr_logistic_n128_c8_d8192", dict(N=128 * 96)),
+]
+
+
+@pytest.mark.parametrize("name,resize", TRAJECTORIES, ids=[t[0] for t in TRAJECTORIES])
+def test_workload_trajectory_matches_oracle(name, resize):
+    w = WORKLOADS[name]
+    if resize:
+        w = w.resized(**resize)
+    _announce("%s N=%d d=%d steps=%d" % (w.name, w.N, w.d, w.steps))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    _check_trajectory(w, X, y, beta0)
+
+
+EDGE = [
+    # ragged partitions (m = 1003) and a masked column tail (d = 1000 on float4 lanes)
+    Workload("edge_cr_lsq_ragged", "CR", "lsq", n=6, c=4, N=6 * 1003, d=1000, lr=0.05, steps=12,
+             policy=POLICY_UNIFORM_COUNT, cap=3, seed=11),
+    # d % 4 != 0: scalar lanes
+    Workload("edge_fr_logistic_d1001", "FR", "logistic", n=6, c=3, N=6 * 777, d=1001, lr=0.1, steps=10,
+             policy=POLICY_UNIFORM_COUNT, cap=2, seed=12),
+    Workload("edge_fr_logistic_d3", "FR", "logistic", n=4, c=2, N=4 * 50, d=3, lr=0.5, steps=8,
+             policy=POLICY_EXACT, cap=1, seed=13),
+    # c = 1 (distributed gradient descent), c = n, n = 1
+    Workload("edge_cr_lsq_c1", "CR", "lsq", n=5, c=1, N=5 * 300, d=256, lr=0.1, steps=6,
+             policy=POLICY_EXACT, cap=0, seed=14),
+    Workload("edge_cr_logistic_c_eq_n", "CR", "logistic", n=4, c=4, N=4 * 333, d=128, lr=0.2, steps=10,
+             policy=POLICY_UNIFORM_COUNT, cap=3, seed=15),
+    Workload("edge_real_c_eq_n", "CR_REAL", "lsq", n=4, c=4, N=4 * 256, d=64, lr=0.02, steps=9,
+             policy=POLICY_UNIFORM_COUNT, cap=3, seed=16, code_seed=16),
+    Workload("edge_single_worker", "FR", "lsq", n=1, c=1, N=517, d=40, lr=0.1, steps=4,
+             policy=POLICY_EXACT, cap=0, seed=17),
+    # the widest rows each lane shape handles
+    Workload("edge_cr_logistic_d16384", "CR", "logistic", n=4, c=2, N=4 * 40, d=16384, lr=0.05, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=18),
+    Workload("edge_fr_lsq_d32768", "FR", "lsq", n=2, c=1, N=2 * 24, d=32768, lr=0.01, steps=3,
+             policy=POLICY_EXACT, cap=0, seed=19),
+    Workload("edge_fr_logistic_d8191", "FR", "logistic", n=4, c=4, N=4 * 37, d=8191, lr=0.05, steps=6,
+             policy=POLICY_UNIFORM_COUNT, cap=3, seed=20),
+    # every worker may straggle up to s = 7 in one step
+    Workload("edge_cr_logistic_heavy", "CR", "logistic", n=16, c=8, N=16 * 64, d=512, lr=0.1, steps=12,
+             policy=POLICY_BERNOULLI, cap=7, p=0.4, seed=21),
+]
+
+
+@pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
+def test_edge_case_trajectory_matches_oracle(w):
+    _announce("%s N=%d d=%d" % (w.name, w.N, w.d))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    _check_trajectory(w, X, y, beta0)
+
+
+def test_unaligned_features_take_the_scalar_path():
+    w = Workload("edge_unaligned", "CR", "lsq", n=4, c=2, N=4 * 200, d=256, lr=0.05, steps=6,
+                 policy=POLICY_EXACT, cap=1, seed=22)
+    _announce(w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    buf = torch.empty(w.N * w.d + 1, device="cuda", dtype=torch.float32)
+    Xu = buf[1:].view(w.N, w.d)
+    Xu.copy_(X)
+    assert Xu.data_ptr() % 16 != 0
+    _check_trajectory(w, Xu, y, beta0, X_host=X.cpu().numpy())
+
+
+def test_runs_are_bitwise_reproducible():
+    w = WORKLOADS["crreal_lsq_n8_c3_d1024"].resized(N=8 * 4096, steps=7)
+    _announce(w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    _, w1 = gpu_run(w, X, y, beta0, masks, keep=())
+    _, w2 = gpu_run(w, X, y, beta0, masks, keep=())
+    assert torch.equal(w1, w2)
+
+
+def test_rejected_step_has_no_effect():
+    w = WORKLOADS["fr_logistic_n4_c2_d64"]
+    _announce("rejected step")
+    X, y, beta0 = make_inputs(w, device="cuda")
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone() + 0.25
+        sess.step(X, y, wv, np.zeros(4, np.uint8), w.lr)
+        before = wv.clone()
+        with pytest.raises(P.PGCError) as e:
+            sess.step(X, y, wv, np.array([1, 1, 0, 0], np.uint8), w.lr)   # a whole FR group straggles
+        assert e.value.status == P.PGC_ESTRAGGLERS
+        torch.cuda.synchronize()
+        assert sess.t == 1
+        assert torch.equal(wv, before)
+    finally:
+        sess.close()
+
+
+# --------------------------------------------------------------------------
+# Full sizes: sampled partitions and properties that hold at any size
+# --------------------------------------------------------------------------
+
+FULL = ["crreal_lsq_n8_c3_d1024", "fr_logistic_n32_c4_d4096", "cr_logistic_n128_c8_d8192"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_ring_holds_partition_gradients(name):
+    """With lr = 0 the weights stay at beta0, so every copy the ring ever holds
+    is g_k(beta0); sampled partitions are compared with the oracle one by one."""
+    w = WORKLOADS[name]
+    _announce("%s full size, lr = 0" % name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone()
+        masks = gpu_masks(w, w.c + 1)
+        for t in range(w.c + 1):
+            sess.step(X, y, wv, masks[t], 0.0)
+        place = sess.placement()
+        m = w.m
+        beta_h = beta0.cpu().numpy().astype(np.float64)
+        for k in sorted({0, w.n // 2, w.n - 1}):
+            Xk = X[k * m:(k + 1) * m].cpu().numpy()
+            yk = y[k * m:(k + 1) * m].cpu().numpy()
+            g = O.partition_gradient(w.model, Xk.astype(np.float64), yk.astype(np.float64), beta_h)
+            holders = [(i, l) for i in range(w.n) for l in range(w.c) if place[i][l] == k]
+            assert len(holders) == w.c
+            for i, l in holders:
+                err = normwise_error(sess.ring(i, l).cpu().numpy(), g)
+                assert err <= FP32_TOL, "partition %d, worker %d slot %d: %.3g" % (k, i, l, err)
+        assert torch.equal(wv, beta0)
+    finally:
+        sess.close()
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_decode_and_update_are_consistent(name):
+    """At full size and the real learning rate: the decoded gradient is the
+    weighted sum of the coded gradients with the library's decode weights, the
+    coded gradients are the sums of the ring copies, and w moves by -lr * ghat."""
+    w = WORKLOADS[name]
+    _announce("%s full size, %d steps" % (name, w.c + 2))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone()
+        B = sess.encoding_matrix()
+        place = sess.placement()
+        for t, mask in enumerate(gpu_masks(w, w.c + 2)):
+            w_before = wv.cpu().numpy().astype(np.float64)
+            sess.step(X, y, wv, mask, w.lr)
+            ghat = sess.decoded().cpu().numpy().astype(np.float64)
+            coded = np.stack([sess.coded(j).cpu().numpy() for j in range(sess.n_coded)]).astype(np.float64)
+            surv, d, scale = sess.decode_coeffs(mask)
+            idx = surv // w.c if w.scheme == "FR" else surv
+            expect = scale * (d[:, None] * coded[idx]).sum(axis=0)
+            assert normwise_error(ghat, expect) <= 1e-6
+            w_after = wv.cpu().numpy().astype(np.float64)
+            assert normwise_error(w_after, w_before - w.lr * ghat) <= 1e-6
+            for j in sorted({0, sess.n_coded - 1}):
+                worker = j * w.c if w.scheme == "FR" else j
+                ring = sum(B[worker, place[worker][l]] * sess.ring(worker, l).cpu().numpy().astype(np.float64)
+                           for l in range(w.c))
+                assert normwise_error(coded[j], ring) <= 1e-6
+    finally:
+        sess.close()
