@@ -67,13 +67,20 @@ enum pgc_mask_policy {
 
 /* Kernels whose GPU time pgc_kernel_time reports. */
 enum pgc_kernel {
-  PGC_KERNEL_GRADIENT = 0, /* per-partition gradient, one HBM pass over the evaluated rows */
-  PGC_KERNEL_REDUCE = 1,   /* per-block partial sums -> ring slots */
-  PGC_KERNEL_CODE = 2,     /* encode + masked decode + update */
-  PGC_KERNEL_COUNT = 3
+  PGC_KERNEL_GRADIENT = 0,    /* linear models: per-partition gradient, one HBM pass over the rows */
+  PGC_KERNEL_REDUCE = 1,      /* per-block partial sums -> ring slots (both model kinds) */
+  PGC_KERNEL_CODE = 2,        /* encode + masked decode + update */
+  PGC_KERNEL_MLP_CAST = 3,    /* MLP: bf16 copies of W1 and W2 */
+  PGC_KERNEL_MLP_FORWARD = 4, /* MLP: H = relu(X W1 + b1), bf16 MFMA GEMM */
+  PGC_KERNEL_MLP_HEAD = 5,    /* MLP: logits, softmax, dZ2, dZ1 and the small-layer gradients */
+  PGC_KERNEL_MLP_WGRAD = 6,   /* MLP: dW1 = X^T dZ1 per partition, bf16 MFMA GEMM */
+  PGC_KERNEL_COUNT = 7
 };
 
 #define PGC_MAX_N 256           /* largest number of workers */
+/* MLP shape limits: d_in % 8 == 0, hidden % 256 == 0, hidden <= 1024, 1 <= classes <= 16. */
+#define PGC_MLP_MAX_HIDDEN 1024
+#define PGC_MLP_MAX_CLASSES 16
 #define PGC_MAX_LINEAR_D 32768  /* largest feature count of the linear models (d % 4 == 0) */
 #define PGC_MAX_LINEAR_D_UNALIGNED 8192 /* ... when d % 4 != 0 or X is not 16-byte aligned */
 
@@ -94,7 +101,8 @@ typedef struct pgc_config {
 int pgc_init(pgc_ctx** out, int scheme, int n, int c, int64_t d);
 
 /* Fix the model and dataset shape.  For the linear models d_in must equal d;
- * for PGC_MLP d must equal d_in*hidden + hidden + hidden*classes + classes.
+ * for PGC_MLP d must equal d_in*hidden + hidden + hidden*classes + classes and
+ * the shape must meet the PGC_MLP_* limits.
  * For PGC_CR_REAL this builds the n x n real-valued encoding matrix from
  * code_seed (PGC_ESINGULAR if a row's defining system is singular).
  * Resets the step counter to 0 and invalidates a bound workspace.  Host only. */

@@ -19,8 +19,14 @@ constexpr size_t kAlign = 256;
 // the problem shape, so results do not depend on the device.
 constexpr int64_t kTargetBlocks = 1024;
 constexpr int64_t kMinRowsPerBlock = 16;
+// MLP head: about this many blocks per launch, rows per block a multiple of 32.
+constexpr int64_t kHeadTargetBlocks = 1024;
+// Ring slots and coded words are padded to a multiple of this many floats so
+// every slot starts 256-byte aligned.
+constexpr int64_t kSlotAlign = 64;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
 struct Grid {
   int32_t n_eval = 0;
@@ -35,6 +41,17 @@ Grid make_grid(int64_t m, int32_t n_eval) {
   b = std::max<int64_t>(1, std::min<int64_t>(b, (m + kMinRowsPerBlock - 1) / kMinRowsPerBlock));
   g.rows_per_block = (m + b - 1) / b;
   g.blocks_per_part = static_cast<int32_t>((m + g.rows_per_block - 1) / g.rows_per_block);
+  return g;
+}
+
+// Head grid of the MLP: blocks of a multiple of 32 rows over the m_pad rows.
+Grid make_head_grid(int64_t m_pad, int32_t n_eval) {
+  Grid g;
+  g.n_eval = n_eval;
+  int64_t b = (kHeadTargetBlocks + n_eval - 1) / n_eval;
+  b = std::max<int64_t>(1, std::min<int64_t>(b, m_pad / 32));
+  g.rows_per_block = round_up((m_pad + b - 1) / b, 32);
+  g.blocks_per_part = static_cast<int32_t>((m_pad + g.rows_per_block - 1) / g.rows_per_block);
   return g;
 }
 
@@ -55,8 +72,12 @@ struct pgc_ctx {
   std::vector<double> coef;   // n_coded x c slot coefficients (real-valued code only)
   // Workspace layout (byte offsets).
   int planes = 0, n_coded = 0;
-  Grid warm, pipe;
+  int64_t ld = 0;             // floats between ring slots / coded words
+  Grid warm, pipe;            // linear gradient grids
+  Grid head_warm, head_pipe;  // MLP head grids
+  int64_t kpad = 0, m_pad = 0, pstride = 0;
   size_t off_ring = 0, off_coded = 0, off_decoded = 0, off_partials = 0, off_coef = 0, ws_need = 0;
+  size_t off_w1t = 0, off_w2t = 0, off_w2p = 0, off_h = 0, off_dz1t = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
@@ -87,24 +108,45 @@ bool is_linear(int model) { return model == PGC_LOGISTIC || model == PGC_LSQ; }
 
 void compute_layout(pgc_ctx* ctx) {
   const int64_t q = ctx->d;
+  const int n = ctx->n;
+  const int32_t n_pipe = ctx->scheme == PGC_FR ? n / ctx->c : n;
   ctx->planes = ctx->scheme == PGC_FR ? 1 : ctx->c;
-  ctx->n_coded = ctx->scheme == PGC_FR ? ctx->n / ctx->c : ctx->n;
-  ctx->warm = make_grid(ctx->m, ctx->n);
-  ctx->pipe = make_grid(ctx->m, ctx->scheme == PGC_FR ? ctx->n / ctx->c : ctx->n);
-  const int64_t max_blocks =
-      std::max<int64_t>(static_cast<int64_t>(ctx->warm.n_eval) * ctx->warm.blocks_per_part,
-                        static_cast<int64_t>(ctx->pipe.n_eval) * ctx->pipe.blocks_per_part);
+  ctx->n_coded = ctx->scheme == PGC_FR ? n / ctx->c : n;
+  ctx->ld = round_up(q, kSlotAlign);
   size_t off = 0;
-  ctx->off_ring = off;
-  off = align_up(off + sizeof(float) * static_cast<size_t>(ctx->planes) * ctx->n * q);
-  ctx->off_coded = off;
-  off = align_up(off + sizeof(float) * static_cast<size_t>(ctx->n_coded) * q);
-  ctx->off_decoded = off;
-  off = align_up(off + sizeof(float) * static_cast<size_t>(q));
-  ctx->off_partials = off;
-  off = align_up(off + sizeof(float) * static_cast<size_t>(max_blocks) * q);
-  ctx->off_coef = off;
-  off = align_up(off + sizeof(double) * ctx->coef.size());
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  ctx->off_ring = take(sizeof(float) * static_cast<size_t>(ctx->planes) * n * ctx->ld);
+  ctx->off_coded = take(sizeof(float) * static_cast<size_t>(ctx->n_coded) * ctx->ld);
+  ctx->off_decoded = take(sizeof(float) * static_cast<size_t>(q));
+  ctx->off_coef = take(sizeof(double) * ctx->coef.size());
+  if (ctx->cfg.model == PGC_MLP) {
+    const int64_t hidden = ctx->cfg.hidden;
+    ctx->kpad = round_up(ctx->cfg.d_in, 32);
+    ctx->m_pad = round_up(ctx->m, 32);
+    ctx->pstride = (pgc::kMlpMaxClasses + 1) * hidden + pgc::kMlpMaxClasses;
+    ctx->head_warm = make_head_grid(ctx->m_pad, n);
+    ctx->head_pipe = make_head_grid(ctx->m_pad, n_pipe);
+    const int64_t head_blocks =
+        std::max<int64_t>(static_cast<int64_t>(ctx->head_warm.n_eval) * ctx->head_warm.blocks_per_part,
+                          static_cast<int64_t>(ctx->head_pipe.n_eval) * ctx->head_pipe.blocks_per_part);
+    ctx->off_w1t = take(2 * static_cast<size_t>(hidden * ctx->kpad));
+    ctx->off_w2t = take(2 * static_cast<size_t>(pgc::kMlpMaxClasses * hidden));
+    ctx->off_w2p = take(2 * static_cast<size_t>(hidden * pgc::kMlpMaxClasses));
+    ctx->off_h = take(2 * static_cast<size_t>(n) * ctx->m * hidden);
+    ctx->off_dz1t = take(2 * static_cast<size_t>(n) * hidden * ctx->m_pad);
+    ctx->off_partials = take(sizeof(float) * static_cast<size_t>(head_blocks * ctx->pstride));
+  } else {
+    ctx->warm = make_grid(ctx->m, n);
+    ctx->pipe = make_grid(ctx->m, n_pipe);
+    const int64_t max_blocks =
+        std::max<int64_t>(static_cast<int64_t>(ctx->warm.n_eval) * ctx->warm.blocks_per_part,
+                          static_cast<int64_t>(ctx->pipe.n_eval) * ctx->pipe.blocks_per_part);
+    ctx->off_partials = take(sizeof(float) * static_cast<size_t>(max_blocks) * q);
+  }
   ctx->ws_need = off;
 }
 
@@ -233,7 +275,14 @@ int pgc_configure(pgc_ctx* ctx, const pgc_config* cfg) {
     if (ctx->d > PGC_MAX_LINEAR_D)
       return fail(ctx, PGC_EINVAL, "d exceeds PGC_MAX_LINEAR_D");
   } else if (cfg->model == PGC_MLP) {
-    return fail(ctx, PGC_EINVAL, "the MLP model is not available in this build");
+    const int64_t d_in = cfg->d_in, hidden = cfg->hidden, classes = cfg->classes;
+    if (d_in < 8 || d_in % 8 != 0) return fail(ctx, PGC_EINVAL, "MLP d_in must be a positive multiple of 8");
+    if (hidden < 256 || hidden % 256 != 0 || hidden > PGC_MLP_MAX_HIDDEN)
+      return fail(ctx, PGC_EINVAL, "MLP hidden must be a multiple of 256 up to PGC_MLP_MAX_HIDDEN");
+    if (classes < 1 || classes > PGC_MLP_MAX_CLASSES)
+      return fail(ctx, PGC_EINVAL, "MLP classes must be in 1..PGC_MLP_MAX_CLASSES");
+    if (ctx->d != d_in * hidden + hidden + hidden * classes + classes)
+      return fail(ctx, PGC_EINVAL, "d must equal d_in*hidden + hidden + hidden*classes + classes");
   } else {
     return fail(ctx, PGC_EINVAL, "unknown model");
   }
@@ -368,6 +417,185 @@ int pgc_get_step(const pgc_ctx* ctx, int64_t* t) {
   return PGC_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Encode + masked decode + update (a6-a8), shared by both model kinds.
+int launch_code_step(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr) {
+  const int c = ctx->c;
+  const bool fr = ctx->scheme == PGC_FR;
+  pgc::CodeArgs ca{};
+  ca.ring = ws_ptr<float>(ctx, ctx->off_ring);
+  ca.coded = ws_ptr<float>(ctx, ctx->off_coded);
+  ca.decoded = ws_ptr<float>(ctx, ctx->off_decoded);
+  ca.w = w;
+  ca.coef = ctx->coef.empty() ? nullptr : ws_ptr<double>(ctx, ctx->off_coef);
+  ca.q = ctx->d;
+  ca.ld = ctx->ld;
+  ca.lr = static_cast<double>(lr);
+  ca.n = ctx->n;
+  ca.c = c;
+  ca.n_coded = ctx->n_coded;
+  ca.fr = fr ? 1 : 0;
+  // FR's coded words are per group (its members' words are identical); CR's per worker.
+  for (size_t m = 0; m < dec.survivors.size(); ++m) {
+    if (dec.d[m] == 0.0) continue;
+    const int j = fr ? dec.survivors[m] / c : dec.survivors[m];
+    ca.a[j] = dec.scale * dec.d[m];
+  }
+  return timed_launch(ctx, PGC_KERNEL_CODE, "code kernel",
+                      [&] { return pgc::launch_code(ca, ctx->stream); });
+}
+
+// a4-a5 for the linear models.
+int linear_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float* w,
+                         int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
+  const bool warm = ctx->t == 0;
+  const Grid& grid = warm ? ctx->warm : ctx->pipe;
+  pgc::LinearGradArgs ga{};
+  ga.X = static_cast<const float*>(X);
+  ga.y = static_cast<const float*>(y);
+  ga.w = w;
+  ga.partials = ws_ptr<float>(ctx, ctx->off_partials);
+  ga.m = ctx->m;
+  ga.rows_per_block = grid.rows_per_block;
+  ga.d = static_cast<int32_t>(ctx->d);
+  ga.blocks_per_part = grid.blocks_per_part;
+  ga.n_eval = grid.n_eval;
+  ga.part_stride = part_stride;
+  ga.part_offset = part_offset;
+  ga.model = ctx->cfg.model;
+  const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
+                         reinterpret_cast<uintptr_t>(w) % 16 == 0;
+
+  pgc::ReduceArgs ra{};
+  ra.partials = ga.partials;
+  ra.ring = ws_ptr<float>(ctx, ctx->off_ring);
+  ra.q = ctx->d;
+  ra.ld = ctx->ld;
+  ra.inv_m = 1.0 / static_cast<double>(ctx->m);
+  ra.n = ctx->n;
+  ra.n_eval = grid.n_eval;
+  ra.blocks_per_part = grid.blocks_per_part;
+  ra.part_stride = part_stride;
+  ra.part_offset = part_offset;
+  ra.plane_first = plane_first;
+  ra.plane_count = plane_count;
+
+  int st = timed_launch(ctx, PGC_KERNEL_GRADIENT, "gradient kernel",
+                        [&] { return pgc::launch_linear_gradient(ga, aligned16, ctx->stream); });
+  if (st != PGC_OK) return st;
+  return timed_launch(ctx, PGC_KERNEL_REDUCE, "reduce kernel",
+                      [&] { return pgc::launch_reduce(ra, ctx->stream); });
+}
+
+// a4-a5 for the MLP: cast, forward, head, weight gradient, small-part reduce,
+// then copies of the slot into the other planes at the CR warm-up.
+int mlp_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float* w,
+                      int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
+  const bool warm = ctx->t == 0;
+  const Grid& hg = warm ? ctx->head_warm : ctx->head_pipe;
+  const int32_t d_in = ctx->cfg.d_in, hidden = ctx->cfg.hidden, classes = ctx->cfg.classes;
+  const int64_t w1 = static_cast<int64_t>(d_in) * hidden;
+  __bf16* W1T = ws_ptr<__bf16>(ctx, ctx->off_w1t);
+  __bf16* W2T = ws_ptr<__bf16>(ctx, ctx->off_w2t);
+  __bf16* W2p = ws_ptr<__bf16>(ctx, ctx->off_w2p);
+  __bf16* H = ws_ptr<__bf16>(ctx, ctx->off_h);
+  __bf16* dZ1T = ws_ptr<__bf16>(ctx, ctx->off_dz1t);
+  float* ring = ws_ptr<float>(ctx, ctx->off_ring);
+  float* partials = ws_ptr<float>(ctx, ctx->off_partials);
+
+  pgc::MlpCastArgs cast{w, W1T, W2T, W2p, d_in, static_cast<int32_t>(ctx->kpad), hidden, classes};
+  pgc::MlpForwardArgs fw{};
+  fw.X = static_cast<const __bf16*>(X);
+  fw.W1T = W1T;
+  fw.b1 = w + w1;
+  fw.H = H;
+  fw.m = ctx->m;
+  fw.d_in = d_in;
+  fw.kpad = static_cast<int32_t>(ctx->kpad);
+  fw.hidden = hidden;
+  fw.n_eval = hg.n_eval;
+  fw.part_stride = part_stride;
+  fw.part_offset = part_offset;
+  pgc::MlpHeadArgs hd{};
+  hd.H = H;
+  hd.y = static_cast<const int32_t*>(y);
+  hd.W2T = W2T;
+  hd.W2p = W2p;
+  hd.b2 = w + w1 + hidden + static_cast<int64_t>(hidden) * classes;
+  hd.dZ1T = dZ1T;
+  hd.partials = partials;
+  hd.m = ctx->m;
+  hd.m_pad = ctx->m_pad;
+  hd.rows_per_block = hg.rows_per_block;
+  hd.inv_m = static_cast<float>(1.0 / static_cast<double>(ctx->m));
+  hd.hidden = hidden;
+  hd.classes = classes;
+  hd.blocks_per_part = hg.blocks_per_part;
+  hd.n_eval = hg.n_eval;
+  hd.part_stride = part_stride;
+  hd.part_offset = part_offset;
+  hd.pstride = static_cast<int32_t>(ctx->pstride);
+  pgc::MlpWgradArgs wg{};
+  wg.X = fw.X;
+  wg.dZ1T = dZ1T;
+  wg.ring = ring;
+  wg.m = ctx->m;
+  wg.m_pad = ctx->m_pad;
+  wg.ld = ctx->ld;
+  wg.d_in = d_in;
+  wg.hidden = hidden;
+  wg.n = ctx->n;
+  wg.plane = plane_first;
+  wg.n_eval = hg.n_eval;
+  wg.part_stride = part_stride;
+  wg.part_offset = part_offset;
+  pgc::MlpReduceArgs rd{};
+  rd.partials = partials;
+  rd.ring = ring;
+  rd.ld = ctx->ld;
+  rd.d_in = d_in;
+  rd.hidden = hidden;
+  rd.classes = classes;
+  rd.n = ctx->n;
+  rd.plane = plane_first;
+  rd.n_eval = hg.n_eval;
+  rd.blocks_per_part = hg.blocks_per_part;
+  rd.part_stride = part_stride;
+  rd.part_offset = part_offset;
+  rd.pstride = static_cast<int32_t>(ctx->pstride);
+
+  int st = timed_launch(ctx, PGC_KERNEL_MLP_CAST, "MLP cast kernels",
+                        [&] { return pgc::launch_mlp_cast(cast, ctx->stream); });
+  if (st == PGC_OK)
+    st = timed_launch(ctx, PGC_KERNEL_MLP_FORWARD, "MLP forward kernel",
+                      [&] { return pgc::launch_mlp_forward(fw, ctx->stream); });
+  if (st == PGC_OK)
+    st = timed_launch(ctx, PGC_KERNEL_MLP_HEAD, "MLP head kernel",
+                      [&] { return pgc::launch_mlp_head(hd, ctx->stream); });
+  if (st == PGC_OK)
+    st = timed_launch(ctx, PGC_KERNEL_MLP_WGRAD, "MLP weight-gradient kernel",
+                      [&] { return pgc::launch_mlp_wgrad(wg, ctx->stream); });
+  if (st == PGC_OK)
+    st = timed_launch(ctx, PGC_KERNEL_REDUCE, "MLP reduce kernel", [&] {
+      hipError_t e = pgc::launch_mlp_reduce(rd, ctx->stream);
+      // CR warm-up: every plane holds the step-0 gradient of each partition.
+      const size_t plane_bytes = sizeof(float) * static_cast<size_t>(ctx->n) * ctx->ld;
+      for (int p = 1; p < plane_count && e == hipSuccess; ++p)
+        e = hipMemcpyAsync(reinterpret_cast<char*>(ring) + (plane_first + p) * plane_bytes,
+                           reinterpret_cast<char*>(ring) + plane_first * plane_bytes, plane_bytes,
+                           hipMemcpyDeviceToDevice, ctx->stream);
+      return e;
+    });
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
 int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
              const uint8_t* straggler_mask, float lr) {
   if (ctx == nullptr) return PGC_EINVAL;
@@ -381,75 +609,35 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
     case pgc::kDecodeSingular: return fail(ctx, PGC_ESINGULAR, err);
     default: break;
   }
-  const int n = ctx->n, c = ctx->c;
-  const int64_t q = ctx->d;
+  const int c = ctx->c;
   const bool fr = ctx->scheme == PGC_FR;
   const bool warm = ctx->t == 0;
-  const Grid& grid = warm ? ctx->warm : ctx->pipe;
   const int o = warm ? 0 : pgc::evaluated_slot(ctx->t, c);
+  // Evaluated partitions: all at the warm-up; one per FR group (jc + o) or
+  // every partition for CR at t >= 1.
+  const int32_t part_stride = (fr && !warm) ? c : 1;
+  const int32_t part_offset = (fr && !warm) ? o : 0;
+  // Ring slot written: FR keeps one slot per partition; CR writes plane o
+  // (worker (k - o) mod n holds partition k in slot o), all planes at t = 0.
+  const int plane_first = fr ? 0 : o;
+  const int plane_count = (!fr && warm) ? c : 1;
 
-  // a4: per-partition gradients of the evaluated partitions.
-  pgc::LinearGradArgs ga{};
-  ga.X = static_cast<const float*>(X);
-  ga.y = static_cast<const float*>(y);
-  ga.w = w;
-  ga.partials = ws_ptr<float>(ctx, ctx->off_partials);
-  ga.m = ctx->m;
-  ga.rows_per_block = grid.rows_per_block;
-  ga.d = static_cast<int32_t>(q);
-  ga.blocks_per_part = grid.blocks_per_part;
-  ga.n_eval = grid.n_eval;
-  ga.part_stride = (fr && !warm) ? c : 1;     // FR evaluates one partition per group
-  ga.part_offset = (fr && !warm) ? o : 0;
-  ga.model = ctx->cfg.model;
-  const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
-                         reinterpret_cast<uintptr_t>(w) % 16 == 0;
-  const pgc::LinearGradShape shape = pgc::linear_grad_shape(ga.d, aligned16);
-  if (!shape.supported)
-    return fail(ctx, PGC_EINVAL, "d = " + std::to_string(q) + " needs d % 4 == 0 and 16-byte aligned X and w");
-
-  // a5: ring write.  FR keeps one slot per partition; CR keeps plane o of
-  // partition k as the copy held by worker (k - o) mod n in slot o.
-  pgc::ReduceArgs ra{};
-  ra.partials = ga.partials;
-  ra.ring = ws_ptr<float>(ctx, ctx->off_ring);
-  ra.q = q;
-  ra.inv_m = 1.0 / static_cast<double>(ctx->m);
-  ra.n = n;
-  ra.n_eval = grid.n_eval;
-  ra.blocks_per_part = grid.blocks_per_part;
-  ra.part_stride = ga.part_stride;
-  ra.part_offset = ga.part_offset;
-  ra.plane_first = fr ? 0 : o;
-  ra.plane_count = (!fr && warm) ? c : 1;
-
-  // a6-a8: encode, masked decode, update.
-  pgc::CodeArgs ca{};
-  ca.ring = ra.ring;
-  ca.coded = ws_ptr<float>(ctx, ctx->off_coded);
-  ca.decoded = ws_ptr<float>(ctx, ctx->off_decoded);
-  ca.w = w;
-  ca.coef = ctx->coef.empty() ? nullptr : ws_ptr<double>(ctx, ctx->off_coef);
-  ca.q = q;
-  ca.lr = static_cast<double>(lr);
-  ca.n = n;
-  ca.c = c;
-  ca.n_coded = ctx->n_coded;
-  ca.fr = fr ? 1 : 0;
-  for (size_t m = 0; m < dec.survivors.size(); ++m) {
-    if (dec.d[m] == 0.0) continue;
-    const int j = fr ? dec.survivors[m] / c : dec.survivors[m];
-    ca.a[j] = dec.scale * dec.d[m];
+  int st;
+  if (ctx->cfg.model == PGC_MLP) {
+    if (reinterpret_cast<uintptr_t>(X) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
+        reinterpret_cast<uintptr_t>(w) % 4 != 0)
+      return fail(ctx, PGC_EINVAL, "MLP: X must be 16-byte aligned, y and w 4-byte aligned");
+    st = mlp_gradient_step(ctx, X, y, w, part_stride, part_offset, plane_first, plane_count);
+  } else {
+    const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
+                           reinterpret_cast<uintptr_t>(w) % 16 == 0;
+    if (!pgc::linear_grad_shape(static_cast<int>(ctx->d), aligned16).supported)
+      return fail(ctx, PGC_EINVAL, "d = " + std::to_string(ctx->d) +
+                                       " needs d % 4 == 0 and 16-byte aligned X and w");
+    st = linear_gradient_step(ctx, X, y, w, part_stride, part_offset, plane_first, plane_count);
   }
-
-  int st = timed_launch(ctx, PGC_KERNEL_GRADIENT, "gradient kernel",
-                        [&] { return pgc::launch_linear_gradient(ga, aligned16, ctx->stream); });
   if (st != PGC_OK) return st;
-  st = timed_launch(ctx, PGC_KERNEL_REDUCE, "reduce kernel",
-                    [&] { return pgc::launch_reduce(ra, ctx->stream); });
-  if (st != PGC_OK) return st;
-  st = timed_launch(ctx, PGC_KERNEL_CODE, "code kernel",
-                    [&] { return pgc::launch_code(ca, ctx->stream); });
+  st = launch_code_step(ctx, dec, w, lr);
   if (st != PGC_OK) return st;
   ctx->t += 1;
   return PGC_OK;
@@ -462,7 +650,7 @@ int pgc_read_ring(const pgc_ctx* ctx, int worker, int slot, float* dev_out) {
     return fail(ctx, PGC_EINVAL, "worker or slot out of range");
   const int k = pgc::held_partition(ctx->scheme, ctx->n, ctx->c, worker, slot);
   const int plane = ctx->scheme == PGC_FR ? 0 : slot;
-  const float* src = ws_ptr<float>(ctx, ctx->off_ring) + (static_cast<int64_t>(plane) * ctx->n + k) * ctx->d;
+  const float* src = ws_ptr<float>(ctx, ctx->off_ring) + (static_cast<int64_t>(plane) * ctx->n + k) * ctx->ld;
   hipError_t e = hipMemcpyAsync(dev_out, src, sizeof(float) * ctx->d, hipMemcpyDeviceToDevice, ctx->stream);
   return e == hipSuccess ? PGC_OK : device_fail(const_cast<pgc_ctx*>(ctx), e, "hipMemcpyAsync");
 }
@@ -471,7 +659,7 @@ int pgc_read_coded(const pgc_ctx* ctx, int index, float* dev_out) {
   if (ctx == nullptr || dev_out == nullptr) return PGC_EINVAL;
   if (ctx->ws == nullptr) return fail(ctx, PGC_ESTATE, "no workspace bound");
   if (index < 0 || index >= ctx->n_coded) return fail(ctx, PGC_EINVAL, "coded index out of range");
-  const float* src = ws_ptr<float>(ctx, ctx->off_coded) + static_cast<int64_t>(index) * ctx->d;
+  const float* src = ws_ptr<float>(ctx, ctx->off_coded) + static_cast<int64_t>(index) * ctx->ld;
   hipError_t e = hipMemcpyAsync(dev_out, src, sizeof(float) * ctx->d, hipMemcpyDeviceToDevice, ctx->stream);
   return e == hipSuccess ? PGC_OK : device_fail(const_cast<pgc_ctx*>(ctx), e, "hipMemcpyAsync");
 }

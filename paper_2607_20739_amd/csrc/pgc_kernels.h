@@ -41,11 +41,13 @@ hipError_t launch_linear_gradient(const LinearGradArgs& a, bool aligned16, hipSt
 
 // ring[(plane_first + p) * n + k][:] = (sum_b partials[e][b][:]) / m for each
 // evaluated e (partition k = e * part_stride + part_offset) and p < plane_count.
-// Sums run in fp64 in block order.
+// Ring slots are ld floats apart (ld >= q, a multiple of 64).  Sums run in
+// fp64 in block order.
 struct ReduceArgs {
   const float* partials;
-  float* ring;             // planes x n x q
+  float* ring;             // planes x n x ld
   int64_t q;
+  int64_t ld;
   double inv_m;
   int32_t n;
   int32_t n_eval;
@@ -65,12 +67,13 @@ hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 // CR: j is a worker, slot(j, o) = plane o, partition (j + o) mod n.
 // coef == nullptr means unit coefficients; else coef[j * c + o] (fp64).
 struct CodeArgs {
-  const float* ring;
-  float* coded;            // n_coded x q
+  const float* ring;       // planes x n x ld
+  float* coded;            // n_coded x ld
   float* decoded;          // q
   float* w;                // q
   const double* coef;      // n_coded x c, or nullptr
   int64_t q;
+  int64_t ld;
   double lr;
   int32_t n;
   int32_t c;
@@ -79,5 +82,79 @@ struct CodeArgs {
   double a[PGC_MAX_N];     // decode weight per coded index (already scaled)
 };
 hipError_t launch_code(const CodeArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Two-layer MLP (d_in -> hidden, ReLU -> classes, softmax cross-entropy), bf16
+// operands with fp32 accumulation on MFMA.  Parameters w (fp32) are laid out
+// W1[d_in][hidden], b1[hidden], W2[hidden][classes], b2[classes].
+// Shape limits: d_in % 8 == 0, hidden % 256 == 0 and <= 1024, classes <= 16.
+// ---------------------------------------------------------------------------
+
+constexpr int kMlpMaxClasses = 16;
+constexpr int kMlpMaxHidden = 1024;
+
+// bf16 copies of the weights for the GEMMs: W1T[hidden][kpad] (zero past d_in),
+// W2T[16][hidden] and W2p[hidden][16] (zero past `classes`).
+struct MlpCastArgs {
+  const float* w;
+  __bf16* W1T;
+  __bf16* W2T;
+  __bf16* W2p;
+  int32_t d_in, kpad, hidden, classes;
+};
+hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s);
+
+// H[e*m + r][h] = bf16(relu(X[k*m + r] . W1[:, h] + b1[h])) for each evaluated
+// partition k = e * part_stride + part_offset, e < n_eval.
+struct MlpForwardArgs {
+  const __bf16* X;
+  const __bf16* W1T;
+  const float* b1;
+  __bf16* H;
+  int64_t m;
+  int32_t d_in, kpad, hidden, n_eval, part_stride, part_offset;
+};
+hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s);
+
+// Per 16-row tile: logits, softmax, dZ2 = (p - onehot(y)) / m, dZ1 = (dZ2 W2^T)
+// masked by H > 0, written transposed to dZ1T[e][h][r] (r < m_pad, zero for
+// r >= m).  Each block writes partial sums of dW2^T[16][hidden], db1[hidden]
+// and db2[16] to partials[(e * blocks_per_part + b) * pstride].
+struct MlpHeadArgs {
+  const __bf16* H;
+  const int32_t* y;
+  const __bf16* W2T;
+  const __bf16* W2p;
+  const float* b2;
+  __bf16* dZ1T;
+  float* partials;
+  int64_t m, m_pad, rows_per_block;
+  float inv_m;
+  int32_t hidden, classes, blocks_per_part, n_eval, part_stride, part_offset, pstride;
+};
+int mlp_head_threads(int hidden);
+hipError_t launch_mlp_head(const MlpHeadArgs& a, hipStream_t s);
+
+// dW1[i][h] = sum_r X[k*m + r][i] dZ1T[e][h][r], written into the ring slot of
+// partition k: ring[((plane * n + k) * ld) + i * hidden + h].
+struct MlpWgradArgs {
+  const __bf16* X;
+  const __bf16* dZ1T;
+  float* ring;
+  int64_t m, m_pad, ld;
+  int32_t d_in, hidden, n, plane, n_eval, part_stride, part_offset;
+};
+hipError_t launch_mlp_wgrad(const MlpWgradArgs& a, hipStream_t s);
+
+// Fold the head partials of each evaluated partition (fp64, block order) into
+// the b1, W2 and b2 parts of its ring slot.
+struct MlpReduceArgs {
+  const float* partials;
+  float* ring;
+  int64_t ld;
+  int32_t d_in, hidden, classes, n, plane, n_eval, blocks_per_part, part_stride, part_offset,
+      pstride;
+};
+hipError_t launch_mlp_reduce(const MlpReduceArgs& a, hipStream_t s);
 
 }  // namespace pgc

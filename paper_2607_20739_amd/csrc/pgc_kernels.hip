@@ -227,7 +227,7 @@ void reduce_kernel(ReduceArgs a) {
   const float g = static_cast<float>(s * a.inv_m);
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
   for (int pl = 0; pl < a.plane_count; ++pl)
-    a.ring[((a.plane_first + pl) * static_cast<int64_t>(a.n) + part) * a.q + col] = g;
+    a.ring[((a.plane_first + pl) * static_cast<int64_t>(a.n) + part) * a.ld + col] = g;
 }
 
 __global__ __launch_bounds__(256)
@@ -240,10 +240,10 @@ void code_kernel(CodeArgs a) {
     for (int o = 0; o < a.c; ++o) {
       const int64_t slot = a.fr ? static_cast<int64_t>(j) * a.c + o
                                 : static_cast<int64_t>(o) * a.n + (j + o) % a.n;
-      const double v = static_cast<double>(a.ring[slot * a.q + col]);
+      const double v = static_cast<double>(a.ring[slot * a.ld + col]);
       word += a.coef ? a.coef[j * a.c + o] * v : v;
     }
-    a.coded[static_cast<int64_t>(j) * a.q + col] = static_cast<float>(word);
+    a.coded[static_cast<int64_t>(j) * a.ld + col] = static_cast<float>(word);
     if (a.a[j] != 0.0) ghat += a.a[j] * word;
   }
   a.decoded[col] = static_cast<float>(ghat);

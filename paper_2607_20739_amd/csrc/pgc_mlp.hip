@@ -1,0 +1,449 @@
+// Two-layer MLP gradient of the PGC step on gfx950: bf16 MFMA with fp32
+// accumulation (the per-partition gradient of Sec. III for a network model;
+// every worker evaluates one partition per step, Sec. IV-A / V-B).
+//
+// Per step, for the evaluated partitions:
+//   cast     w (fp32) -> W1T, W2T, W2p (bf16 copies laid out for the MFMAs)
+//   forward  H = relu(X W1 + b1)                       MFMA 16x16x32, LDS-tiled
+//   head     logits = H W2 + b2, softmax, dZ2 = (p - onehot) / m,
+//            dZ1 = (dZ2 W2^T) * [H > 0] (stored transposed), and block
+//            partials of dW2 = H^T dZ2, db1, db2         MFMA 16x16x32 / 16x16x16
+//   wgrad    dW1 = X^T dZ1 straight into the ring slot  MFMA 16x16x32, X tile
+//            transposed through LDS
+//   reduce   head partials -> b1, W2, b2 parts of the ring slot (fp64, fixed order)
+//
+// MFMA lane layouts (gfx950, wave64; l = lane, lr = l % 16, lg = l / 16):
+//   16x16x32 bf16: A[lr][8 lg + j], B[8 lg + j][lr], j < 8;  D[4 lg + i][lr]
+//   16x16x16 bf16: A[lr][4 lg + j], B[4 lg + j][lr], j < 4;  D[4 lg + i][lr]
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "pgc_kernels.h"
+
+namespace pgc {
+namespace {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma_k32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_k16(bf16x4 a, bf16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+template <class T>
+__device__ __forceinline__ T load_vec(const bf16* p) { return *reinterpret_cast<const T*>(p); }
+
+// ---------------------------------------------------------------------------
+// cast
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256)
+void mlp_cast_w1_kernel(MlpCastArgs a) {
+  __shared__ float tile[32][33];
+  const int i0 = blockIdx.x * 32, h0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int j = ty; j < 32; j += 8) {
+    const int i = i0 + j;
+    tile[j][tx] = i < a.d_in ? a.w[static_cast<int64_t>(i) * a.hidden + h0 + tx] : 0.0f;
+  }
+  __syncthreads();
+  for (int j = ty; j < 32; j += 8)
+    a.W1T[static_cast<int64_t>(h0 + j) * a.kpad + i0 + tx] = static_cast<bf16>(tile[tx][j]);
+}
+
+__global__ __launch_bounds__(256)
+void mlp_cast_w2_kernel(MlpCastArgs a) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.hidden * kMlpMaxClasses) return;
+  const int h = idx / kMlpMaxClasses, c = idx % kMlpMaxClasses;
+  const int64_t w2 = static_cast<int64_t>(a.d_in) * a.hidden + a.hidden;
+  const float v = c < a.classes ? a.w[w2 + static_cast<int64_t>(h) * a.classes + c] : 0.0f;
+  a.W2T[static_cast<int64_t>(c) * a.hidden + h] = static_cast<bf16>(v);
+  a.W2p[idx] = static_cast<bf16>(v);
+}
+
+// ---------------------------------------------------------------------------
+// forward: H = relu(X W1 + b1), block tile 128 rows x 256 hidden, K step 32,
+// 4 waves as 2 x 2 (64 x 128 each), double-buffered LDS.
+// ---------------------------------------------------------------------------
+
+constexpr int kFwBM = 128, kFwBN = 256, kFwBK = 32, kFwLd = kFwBK + 8;
+
+__global__ __launch_bounds__(256)
+void mlp_forward_kernel(MlpForwardArgs a) {
+  __shared__ bf16 As[2][kFwBM][kFwLd];
+  __shared__ bf16 Bs[2][kFwBN][kFwLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int h0 = blockIdx.x * kFwBN;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kFwBM;
+  const int e = blockIdx.z;
+  const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
+  const bf16* Xp = a.X + part * a.m * a.d_in;
+  const int ksteps = a.kpad / kFwBK;
+  const int dchunks = a.d_in / 8;
+
+  bf16x8 ra[2], rb[4];
+  auto fetch = [&](int ks) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = tid + u * 256, row = idx >> 2, ch = idx & 3;
+      const int kc = ks * 4 + ch;
+      const int64_t gr = r0 + row;
+      ra[u] = (gr < a.m && kc < dchunks) ? load_vec<bf16x8>(Xp + gr * a.d_in + kc * 8) : bf16x8{};
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * 256, row = idx >> 2, ch = idx & 3;
+      rb[u] = load_vec<bf16x8>(a.W1T + static_cast<int64_t>(h0 + row) * a.kpad + ks * kFwBK + ch * 8);
+    }
+  };
+  auto stage = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = tid + u * 256;
+      *reinterpret_cast<bf16x8*>(&As[buf][idx >> 2][(idx & 3) * 8]) = ra[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * 256;
+      *reinterpret_cast<bf16x8*>(&Bs[buf][idx >> 2][(idx & 3) * 8]) = rb[u];
+    }
+  };
+
+  f32x4 acc[4][8];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = f32x4{};
+
+  fetch(0);
+  stage(0);
+  __syncthreads();
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int buf = ks & 1;
+    if (ks + 1 < ksteps) fetch(ks + 1);
+    bf16x8 af[4], bfr[8];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+      af[mt] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * 64 + mt * 16 + lr][lg * 8]);
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt)
+      bfr[nt] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * 128 + nt * 16 + lr][lg * 8]);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = mfma_k32(af[mt], bfr[nt], acc[mt][nt]);
+    if (ks + 1 < ksteps) stage(buf ^ 1);
+    __syncthreads();
+  }
+
+  bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * a.hidden;
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) {
+    const int h = h0 + wn * 128 + nt * 16 + lr;
+    const float bias = a.b1[h];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t row = r0 + wm * 64 + mt * 16 + lg * 4 + i;
+        if (row < a.m) Hp[row * a.hidden + h] = static_cast<bf16>(fmaxf(acc[mt][nt][i] + bias, 0.0f));
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// head: one wave per 128 hidden columns, 16-row tiles; the wave's partial
+// logits are summed across waves through LDS in wave order.
+// ---------------------------------------------------------------------------
+
+constexpr int kHeadCols = 128;
+constexpr int kHeadMaxWaves = kMlpMaxHidden / kHeadCols;
+
+__global__ __launch_bounds__(64 * kHeadMaxWaves)
+void mlp_head_kernel(MlpHeadArgs a) {
+  __shared__ float zpart[2][kHeadMaxWaves][16][16];
+  __shared__ float dzt[kHeadMaxWaves][16][17];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int waves = a.hidden / kHeadCols;
+  const int e = blockIdx.y;
+  const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
+  const int hw0 = wave * kHeadCols;
+  const int64_t hidden = a.hidden;
+  const bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * hidden;
+  const int32_t* yp = a.y + part * a.m;
+  bf16* dz1 = a.dZ1T + static_cast<int64_t>(e) * hidden * a.m_pad;
+  const int64_t rbeg = static_cast<int64_t>(blockIdx.x) * a.rows_per_block;
+  const int64_t rend = min(rbeg + a.rows_per_block, a.m_pad);
+
+  bf16x8 w2t[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) w2t[ks] = load_vec<bf16x8>(a.W2T + lr * hidden + hw0 + ks * 32 + lg * 8);
+  bf16x4 w2p[8];
+#pragma unroll
+  for (int ht = 0; ht < 8; ++ht) w2p[ht] = load_vec<bf16x4>(a.W2p + (hw0 + ht * 16 + lr) * 16 + lg * 4);
+  const float b2 = lr < a.classes ? a.b2[lr] : 0.0f;
+
+  f32x4 dw2[8];
+  float db1[8][4];
+#pragma unroll
+  for (int ht = 0; ht < 8; ++ht) {
+    dw2[ht] = f32x4{};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) db1[ht][i] = 0.0f;
+  }
+  float db2 = 0.0f;
+  int buf = 0;
+  for (int64_t r0 = rbeg; r0 < rend; r0 += 16) {
+    // Partial logits of rows r0..r0+15 over this wave's hidden columns.
+    const int64_t row_l = r0 + lr;
+    const bool valid_l = row_l < a.m;
+    f32x4 z = f32x4{};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const bf16x8 hv = valid_l ? load_vec<bf16x8>(Hp + row_l * hidden + hw0 + ks * 32 + lg * 8) : bf16x8{};
+      z = mfma_k32(hv, w2t[ks], z);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) zpart[buf][wave][lg * 4 + i][lr] = z[i];
+    __syncthreads();
+    // Softmax over the classes of rows r0 + 4 lg + i (class lr on this lane).
+    float dz2[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = 0.0f;
+      for (int w = 0; w < waves; ++w) s += zpart[buf][w][lg * 4 + i][lr];
+      const int64_t row = r0 + lg * 4 + i;
+      const bool live = lr < a.classes;
+      const float v = live ? s + b2 : -INFINITY;
+      float mx = v;
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      const float ex = live ? expf(v - mx) : 0.0f;
+      float sum = ex;
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+      const int label = row < a.m ? yp[row] : -1;
+      dz2[i] = (row < a.m && live) ? (ex / sum - (lr == label ? 1.0f : 0.0f)) * a.inv_m : 0.0f;
+      db2 += dz2[i];
+    }
+    buf ^= 1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dzt[wave][lg * 4 + i][lr] = dz2[i];
+    __syncthreads();
+    bf16x4 dz_b, dz_a;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dz_b[j] = static_cast<bf16>(dzt[wave][lr][lg * 4 + j]);   // dZ2[r0 + lr][4 lg + j]
+      dz_a[j] = static_cast<bf16>(dz2[j]);                     // dZ2[r0 + 4 lg + j][lr]
+    }
+#pragma unroll
+    for (int ht = 0; ht < 8; ++ht) {
+      const int h = hw0 + ht * 16;
+      // dH^T[h + 4 lg + i][r0 + lr] = sum_c W2[h + 4 lg + i][c] dZ2[r0 + lr][c]
+      const f32x4 dh = mfma_k16(w2p[ht], dz_b, f32x4{});
+      const bf16x4 hm = valid_l ? load_vec<bf16x4>(Hp + row_l * hidden + h + lg * 4) : bf16x4{};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float g = static_cast<float>(hm[i]) > 0.0f ? dh[i] : 0.0f;
+        db1[ht][i] += g;
+        dz1[(h + lg * 4 + i) * a.m_pad + row_l] = static_cast<bf16>(g);
+      }
+      // dW2^T[4 lg + i][h + lr] += sum_r dZ2[r][4 lg + i] H[r][h + lr]
+      bf16x4 hb;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t rr = r0 + lg * 4 + j;
+        hb[j] = rr < a.m ? Hp[rr * hidden + h + lr] : static_cast<bf16>(0.0f);
+      }
+      dw2[ht] = mfma_k16(dz_a, hb, dw2[ht]);
+    }
+  }
+
+  float* out = a.partials + (static_cast<int64_t>(e) * a.blocks_per_part + blockIdx.x) * a.pstride;
+#pragma unroll
+  for (int ht = 0; ht < 8; ++ht) {
+    const int h = hw0 + ht * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      out[(lg * 4 + i) * hidden + h + lr] = dw2[ht][i];
+      float s = db1[ht][i];
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off, 64);
+      if (lr == 0) out[kMlpMaxClasses * hidden + h + lg * 4 + i] = s;
+    }
+  }
+  if (wave == 0) {
+    float s = db2;
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    if (lane < 16) out[(kMlpMaxClasses + 1) * hidden + lane] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// wgrad: dW1^T tile 256 hidden x 112 features per block, K = rows in steps of
+// 32; 4 waves, each 64 hidden x 112 features.  dZ1T rows feed the A operand
+// straight from global memory; the X tile is transposed into LDS.
+// ---------------------------------------------------------------------------
+
+constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 32, kWgLd = kWgBK + 8;
+
+__global__ __launch_bounds__(256)
+void mlp_wgrad_kernel(MlpWgradArgs a) {
+  __shared__ bf16 XT[2][kWgBN][kWgLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int e = blockIdx.z;
+  const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
+  const int hb0 = blockIdx.x * kWgBM + wave * 64;
+  const int i0 = blockIdx.y * kWgBN;
+  const bf16* Xp = a.X + part * a.m * a.d_in;
+  const bf16* dz = a.dZ1T + static_cast<int64_t>(e) * a.hidden * a.m_pad;
+  const int ksteps = static_cast<int>(a.m_pad / kWgBK);
+  const int dchunks = a.d_in / 8;
+
+  // X staging: thread t < 224 moves rows (2 rp, 2 rp + 1) x features fc*8..+7.
+  const bool stager = tid < (kWgBK / 2) * (kWgBN / 8);
+  const int rp = tid / (kWgBN / 8), fc = tid % (kWgBN / 8);
+  const bool fvalid = stager && (i0 / 8 + fc) < dchunks;
+  bf16x8 x0 = bf16x8{}, x1 = bf16x8{};
+  auto fetch_x = [&](int ks) {
+    if (!fvalid) return;
+    const int64_t r = static_cast<int64_t>(ks) * kWgBK + 2 * rp;
+    x0 = r < a.m ? load_vec<bf16x8>(Xp + r * a.d_in + i0 + fc * 8) : bf16x8{};
+    x1 = r + 1 < a.m ? load_vec<bf16x8>(Xp + (r + 1) * a.d_in + i0 + fc * 8) : bf16x8{};
+  };
+  auto stage_x = [&](int buf) {
+    if (!stager) return;
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      bf16x2 pair;
+      pair[0] = x0[f];
+      pair[1] = x1[f];
+      *reinterpret_cast<bf16x2*>(&XT[buf][fc * 8 + f][2 * rp]) = pair;
+    }
+  };
+  bf16x8 av[4];
+  auto fetch_a = [&](int ks) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+      av[mt] = load_vec<bf16x8>(dz + static_cast<int64_t>(hb0 + mt * 16 + lr) * a.m_pad + ks * kWgBK + lg * 8);
+  };
+
+  f32x4 acc[4][7];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 7; ++nt) acc[mt][nt] = f32x4{};
+
+  fetch_x(0);
+  stage_x(0);
+  fetch_a(0);
+  __syncthreads();
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int buf = ks & 1;
+    bf16x8 af[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) af[mt] = av[mt];
+    if (ks + 1 < ksteps) {
+      fetch_x(ks + 1);
+      fetch_a(ks + 1);
+    }
+#pragma unroll
+    for (int nt = 0; nt < 7; ++nt) {
+      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&XT[buf][nt * 16 + lr][lg * 8]);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt], bv, acc[mt][nt]);
+    }
+    if (ks + 1 < ksteps) stage_x(buf ^ 1);
+    __syncthreads();
+  }
+
+  float* slot = a.ring + (static_cast<int64_t>(a.plane) * a.n + part) * a.ld;
+#pragma unroll
+  for (int nt = 0; nt < 7; ++nt) {
+    const int feat = i0 + nt * 16 + lr;
+    if (feat >= a.d_in) continue;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+      *reinterpret_cast<f32x4*>(slot + static_cast<int64_t>(feat) * a.hidden + hb0 + mt * 16 + lg * 4) =
+          acc[mt][nt];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// reduce: head partials -> ring (b1, W2 in [hidden][classes] order, b2)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256)
+void mlp_reduce_kernel(MlpReduceArgs a) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= a.pstride) return;
+  const int e = blockIdx.y;
+  const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
+  const float* p = a.partials + static_cast<int64_t>(e) * a.blocks_per_part * a.pstride + j;
+  double s = 0.0;
+  for (int b = 0; b < a.blocks_per_part; ++b) s += static_cast<double>(p[static_cast<int64_t>(b) * a.pstride]);
+  float* slot = a.ring + (static_cast<int64_t>(a.plane) * a.n + part) * a.ld;
+  const int64_t w1 = static_cast<int64_t>(a.d_in) * a.hidden;
+  const int hw = kMlpMaxClasses * a.hidden;
+  if (j < hw) {
+    const int c = j / a.hidden, h = j % a.hidden;
+    if (c < a.classes) slot[w1 + a.hidden + static_cast<int64_t>(h) * a.classes + c] = static_cast<float>(s);
+  } else if (j < hw + a.hidden) {
+    slot[w1 + (j - hw)] = static_cast<float>(s);
+  } else {
+    const int c = j - hw - a.hidden;
+    if (c < a.classes)
+      slot[w1 + a.hidden + static_cast<int64_t>(a.hidden) * a.classes + c] = static_cast<float>(s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(mlp_cast_w1_kernel, dim3(a.kpad / 32, a.hidden / 32), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mlp_cast_w2_kernel, dim3((a.hidden * kMlpMaxClasses + 255) / 256), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s) {
+  dim3 grid(a.hidden / kFwBN, static_cast<unsigned>((a.m + kFwBM - 1) / kFwBM), a.n_eval);
+  hipLaunchKernelGGL(mlp_forward_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+int mlp_head_threads(int hidden) { return 64 * (hidden / kHeadCols); }
+
+hipError_t launch_mlp_head(const MlpHeadArgs& a, hipStream_t s) {
+  dim3 grid(a.blocks_per_part, a.n_eval);
+  hipLaunchKernelGGL(mlp_head_kernel, grid, dim3(mlp_head_threads(a.hidden)), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mlp_wgrad(const MlpWgradArgs& a, hipStream_t s) {
+  dim3 grid(a.hidden / kWgBM, (a.d_in + kWgBN - 1) / kWgBN, a.n_eval);
+  hipLaunchKernelGGL(mlp_wgrad_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mlp_reduce(const MlpReduceArgs& a, hipStream_t s) {
+  dim3 grid((a.pstride + 255) / 256, a.n_eval);
+  hipLaunchKernelGGL(mlp_reduce_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace pgc

@@ -1,0 +1,139 @@
+"""GPU parity of the two-layer MLP path (bf16 MFMA) against the fp64 oracle.
+
+The oracle evaluates the network with the same bf16 inputs and bf16-rounded
+W1, W2 (reading R3); the GPU additionally rounds H, dZ2 and dZ1 to bf16 for
+its MFMAs, which the 2e-2 normwise bar covers.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_20739_amd as P
+from oracle import pgc_oracle as O
+from workloads import WORKLOADS, Workload, make_inputs, POLICY_BERNOULLI, POLICY_EXACT, \
+    POLICY_UNIFORM_COUNT
+
+from _parity import gpu_masks, gpu_run, gpu_session, normwise_error, oracle_masks, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+
+
+def _announce(what):
+    print("\n[gpu case] " + what, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    P.lib()
+
+
+def _host_inputs(X, y, beta0):
+    return X.float().cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy()
+
+
+def _check_trajectory(w):
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks_gpu = gpu_masks(w)
+    masks_or = oracle_masks(w)
+    assert [m.tolist() for m in masks_gpu] == [m.tolist() for m in masks_or]
+    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu)
+    recs_or = oracle_run(w, *_host_inputs(X, y, beta0), masks_or)
+    worst = 0.0
+    for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
+        assert np.all(np.isfinite(g["ghat"])) and np.all(np.isfinite(g["w"]))
+        e_g = normwise_error(g["ghat"], o.ghat)
+        e_w = normwise_error(g["w"], o.beta)
+        worst = max(worst, e_g, e_w)
+        assert e_g <= BF16_TOL, "step %d: decoded gradient error %.3g" % (t, e_g)
+        assert e_w <= BF16_TOL, "step %d: weight error %.3g" % (t, e_w)
+    print("  worst normwise error over %d steps: %.3g" % (len(recs_gpu), worst), flush=True)
+
+
+SMALL = [
+    # ragged partitions (m = 100, padded to 128 rows) and two classes short of 16
+    Workload("mlp_cr_small_ragged", "CR", "mlp", n=4, c=2, N=4 * 100, d=64, lr=0.05, steps=6,
+             policy=POLICY_EXACT, cap=1, seed=31, hidden=256, classes=10),
+    # d_in not a multiple of the K step (40 = 32 + 8), three classes, FR
+    Workload("mlp_fr_small", "FR", "mlp", n=4, c=2, N=4 * 64, d=40, lr=0.05, steps=6,
+             policy=POLICY_EXACT, cap=1, seed=32, hidden=256, classes=3),
+    # hidden = 512 (two forward column blocks, four head waves), c = n
+    Workload("mlp_cr_c_eq_n", "CR", "mlp", n=3, c=3, N=3 * 160, d=120, lr=0.02, steps=7,
+             policy=POLICY_UNIFORM_COUNT, cap=2, seed=33, hidden=512, classes=16),
+    # the real-valued code on the MLP
+    Workload("mlp_real_code", "CR_REAL", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.02, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=34, hidden=256, classes=10, code_seed=3),
+]
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_small_mlp_trajectory_matches_oracle(w):
+    _announce("%s N=%d d_in=%d hidden=%d" % (w.name, w.N, w.d, w.hidden))
+    _check_trajectory(w)
+
+
+def test_mlp_workload_shape_trajectory_matches_oracle():
+    """The 784 -> 1024 -> 10 network, n = 64, c = 4, with 256 rows per partition."""
+    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"].resized(N=64 * 256)
+    _announce("%s N=%d" % (w.name, w.N))
+    _check_trajectory(w)
+
+
+def test_mlp_runs_are_bitwise_reproducible():
+    w = SMALL[0]
+    _announce("mlp reproducibility")
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    _, w1 = gpu_run(w, X, y, beta0, masks, keep=())
+    _, w2 = gpu_run(w, X, y, beta0, masks, keep=())
+    assert torch.equal(w1, w2)
+
+
+def test_full_size_mlp_ring_holds_partition_gradients():
+    """Full size (N = 1048576), lr = 0: sampled partitions' ring copies equal the
+    oracle's gradient at beta0, computed one partition at a time."""
+    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+    _announce("%s full size, lr = 0" % w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone()
+        for mask in gpu_masks(w, w.c + 1):
+            sess.step(X, y, wv, mask, 0.0)
+        place = sess.placement()
+        beta_h = beta0.cpu().numpy().astype(np.float64)
+        shape = (w.d, w.hidden, w.classes)
+        for k in (0, w.n // 2, w.n - 1):
+            rows = slice(k * w.m, (k + 1) * w.m)
+            g = O.partition_gradient(O.MLP, X[rows].float().cpu().numpy().astype(np.float64),
+                                     y[rows].cpu().numpy(), beta_h, shape)
+            for i, l in [(i, l) for i in range(w.n) for l in range(w.c) if place[i][l] == k]:
+                err = normwise_error(sess.ring(i, l).cpu().numpy(), g)
+                assert err <= BF16_TOL, "partition %d, worker %d slot %d: %.3g" % (k, i, l, err)
+        assert torch.equal(wv, beta0)
+    finally:
+        sess.close()
+
+
+def test_full_size_mlp_decode_and_update_are_consistent():
+    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+    _announce("%s full size, %d steps" % (w.name, 3))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone()
+        for mask in gpu_masks(w, 3):
+            w_before = wv.cpu().numpy().astype(np.float64)
+            sess.step(X, y, wv, mask, w.lr)
+            ghat = sess.decoded().cpu().numpy().astype(np.float64)
+            surv, d, scale = sess.decode_coeffs(mask)
+            acc = np.zeros_like(ghat)
+            for dm, j in zip(d, surv):
+                acc += dm * sess.coded(int(j)).cpu().numpy().astype(np.float64)
+            assert normwise_error(ghat, scale * acc) <= 1e-5
+            assert normwise_error(wv.cpu().numpy().astype(np.float64), w_before - w.lr * ghat) <= 1e-6
+    finally:
+        sess.close()
