@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
 DEFAULT_WORKLOAD = "crreal_lsq_n8_c3_d1024"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_kernels.hip")
@@ -47,19 +48,29 @@ def rows_per_step(w):
 def algorithmic_bytes(w):
     """(gradient-kernel bytes per launch, whole-step bytes) of a pipelined step.
 
-    Gradient kernel: each evaluated row once (4d bytes of features + 4 of label)
-    plus w.  Whole step adds the fresh-gradient writes, one read of every ring
-    slot the encode combines, the coded-gradient writes, the decoded vector and
-    the update's read and write of w.
+    Linear models: each evaluated row once (4d bytes of features + 4 of label)
+    plus w.  MLP: each evaluated row's bf16 features and int32 label.  The
+    whole step adds the fresh-gradient writes, one read of every ring slot the
+    encode combines, the coded-gradient writes, the decoded vector and the
+    update's read and write of w.
     """
     q = w.q
     rows = rows_per_step(w)
     n_eval = w.n // w.c if w.scheme == "FR" else w.n
     planes_read = w.n if w.scheme == "FR" else w.n * w.c
     n_coded = w.n // w.c if w.scheme == "FR" else w.n
-    grad = rows * (4 * w.d + 4) + 4 * q
+    if w.model == "mlp":
+        grad = rows * (2 * w.d + 4) + 4 * q
+    else:
+        grad = rows * (4 * w.d + 4) + 4 * q
     step = grad + 4 * q * (n_eval + planes_read + n_coded + 1 + 2)
     return grad, step
+
+
+def mlp_gemm_flops(w):
+    """Algorithmic FLOPs of one launch of the forward (X W1) or the weight-gradient
+    (X^T dZ1) GEMM: 2 * rows * d_in * hidden each."""
+    return 2.0 * rows_per_step(w) * w.d * w.hidden
 
 
 def read_traffic(workload):
@@ -86,12 +97,13 @@ def cpu_baseline(w, X, y, beta0, budget_s):
     if w.scheme == "CR_REAL":
         B = O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
     max_steps = 100000
-    Xh, yh, bh = X.cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy()
+    Xh, yh, bh = X.float().cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy()
+    shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
 
     def run(steps):
         masks = [R.straggler_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(steps)]
         t0 = time.perf_counter()
-        O.run(schemes[w.scheme], w.model, w.n, w.c, Xh, yh, bh, w.lr, masks, B=B,
+        O.run(schemes[w.scheme], w.model, w.n, w.c, Xh, yh, bh, w.lr, masks, B=B, shape=shape,
               keep_coded=False, keep_alpha=False)
         return time.perf_counter() - t0
 
@@ -128,6 +140,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="wall-time budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--all-kernel-times", action="store_true",
+                    help="time every kernel with HIP events (adds event overhead to the step)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 20 times and exit "
                          "(a known-size reference for the HBM byte counters)")
@@ -168,7 +182,12 @@ def main():
     stream = torch.cuda.current_stream(dev)
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
-    P.pgc_set_timing(sess.ctx, True)
+    # HIP events bracket only the dominant kernel(s) inside the timed region.
+    timed_kernels = ([P.PGC_KERNEL_MLP_FORWARD, P.PGC_KERNEL_MLP_WGRAD] if w.model == "mlp"
+                     else [P.PGC_KERNEL_GRADIENT])
+    if args.all_kernel_times:
+        timed_kernels = True
+    P.pgc_set_timing(sess.ctx, timed_kernels)
     torch.cuda.synchronize()
     start.record(stream)
     for t in range(args.warmup, total):
@@ -176,10 +195,15 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     elapsed_ms = start.elapsed_time(stop)
-    grad_ms, grad_launches = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_GRADIENT)
-    red_ms, _ = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_REDUCE)
-    code_ms, _ = P.pgc_kernel_time(sess.ctx, P.PGC_KERNEL_CODE)
-    P.pgc_set_timing(sess.ctx, False)
+    kernels = {"gradient": P.PGC_KERNEL_GRADIENT, "reduce": P.PGC_KERNEL_REDUCE, "code": P.PGC_KERNEL_CODE,
+               "mlp_cast": P.PGC_KERNEL_MLP_CAST, "mlp_forward": P.PGC_KERNEL_MLP_FORWARD,
+               "mlp_head": P.PGC_KERNEL_MLP_HEAD, "mlp_wgrad": P.PGC_KERNEL_MLP_WGRAD}
+    per_launch = {}
+    for name, kid in kernels.items():
+        ms, launches = P.pgc_kernel_time(sess.ctx, kid)
+        if launches:
+            per_launch[name] = ms / launches
+    P.pgc_set_timing(sess.ctx, [])
     if not bool(torch.isfinite(wv).all()):
         print("non-finite weights after the timed steps", file=sys.stderr)
         return 1
@@ -187,11 +211,19 @@ def main():
     ms_per_step = elapsed_ms / args.steps
     steps_per_s = 1000.0 / ms_per_step
     grad_bytes, step_bytes = algorithmic_bytes(w)
-    grad_avg_ms = grad_ms / grad_launches
-    achieved = grad_bytes / (grad_avg_ms * 1e-3) / 1e9
-    traffic = read_traffic(w.name)
-    log("step %.4f ms; gradient %.4f ms, reduce %.4f ms, code %.4f ms per launch"
-        % (ms_per_step, grad_avg_ms, red_ms / args.steps, code_ms / args.steps))
+    if w.model == "mlp":
+        dominant = max(("mlp_forward", "mlp_wgrad"), key=lambda k: per_launch[k])
+        achieved = mlp_gemm_flops(w) / (per_launch[dominant] * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "kernel": dominant, "achieved": achieved,
+                    "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": read_traffic(w.name)}
+    else:
+        achieved = grad_bytes / (per_launch["gradient"] * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": "linear_gradient_kernel", "achieved": achieved,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                    "traffic": read_traffic(w.name)}
+    log("step %.4f ms; per launch (ms): %s" % (ms_per_step, ", ".join(
+        "%s %.4f" % kv for kv in per_launch.items())))
 
     baseline = None
     if args.cpu_seconds > 0:
@@ -210,17 +242,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if w.model == "mlp" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "scheme": w.scheme, "loss": w.model, "n": w.n, "c": w.c,
-                   "N": w.N, "d": w.d, "lr": w.lr},
+                   "N": w.N, "d": w.d, "q": w.q, "lr": w.lr},
         "samples_per_s": {"unique_rows": rows * steps_per_s, "worker_samples": w.N * steps_per_s},
         "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
-        "kernel_ms_per_step": {"gradient": grad_avg_ms, "reduce": red_ms / args.steps,
-                               "code": code_ms / args.steps},
-        "roofline": {"bound": "hbm", "kernel": "linear_gradient_kernel", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic},
+        "kernel_ms_per_launch": per_launch,
+        "roofline": roofline,
         "cpu_baseline": baseline,
     }
     print(json.dumps(out), flush=True)

@@ -68,8 +68,9 @@ enum pgc_mask_policy {
 /* Kernels whose GPU time pgc_kernel_time reports. */
 enum pgc_kernel {
   PGC_KERNEL_GRADIENT = 0,    /* linear models: per-partition gradient, one HBM pass over the rows */
-  PGC_KERNEL_REDUCE = 1,      /* per-block partial sums -> ring slots (both model kinds) */
-  PGC_KERNEL_CODE = 2,        /* encode + masked decode + update */
+  PGC_KERNEL_REDUCE = 1,      /* MLP: head partial sums -> ring slots */
+  PGC_KERNEL_CODE = 2,        /* encode + masked decode + update (linear models: also folds the
+                                 gradient kernel's partial sums into the ring first) */
   PGC_KERNEL_MLP_CAST = 3,    /* MLP: bf16 copies of W1 and W2 */
   PGC_KERNEL_MLP_FORWARD = 4, /* MLP: H = relu(X W1 + b1), bf16 MFMA GEMM */
   PGC_KERNEL_MLP_HEAD = 5,    /* MLP: logits, softmax, dZ2, dZ1 and the small-layer gradients */
@@ -189,10 +190,11 @@ int pgc_read_decoded(const pgc_ctx* ctx, float* dev_out);
 int pgc_get_step(const pgc_ctx* ctx, int64_t* t);
 
 /* Per-kernel GPU timing with HIP events recorded around each launch on the
- * context stream.  pgc_set_timing(ctx, 1) enables and clears the totals;
- * pgc_kernel_time synchronises on the recorded events and returns the summed
- * milliseconds and launch count of `kernel` (enum pgc_kernel) since enabling. */
-int pgc_set_timing(pgc_ctx* ctx, int enable);
+ * context stream.  pgc_set_timing(ctx, mask) times the kernels whose bit
+ * (1 << enum pgc_kernel) is set in `mask` (0 disables timing, -1 times all)
+ * and clears the totals; pgc_kernel_time synchronises on the recorded events
+ * and returns the summed milliseconds and launch count of `kernel` since. */
+int pgc_set_timing(pgc_ctx* ctx, int kernel_mask);
 int pgc_kernel_time(pgc_ctx* ctx, int kernel, double* total_ms, int64_t* launches);
 
 /* Text of a status code; last error message of a context (never NULL). */

@@ -18,6 +18,7 @@ PGC_LOGISTIC, PGC_LSQ, PGC_MLP = 0, 1, 2
 PGC_OK, PGC_EINVAL, PGC_ESTRAGGLERS, PGC_ESINGULAR, PGC_EDEVICE, PGC_ESTATE = 0, -1, -2, -3, -4, -5
 PGC_POLICY_EXACT, PGC_POLICY_UNIFORM_COUNT, PGC_POLICY_BERNOULLI = 0, 1, 2
 PGC_KERNEL_GRADIENT, PGC_KERNEL_REDUCE, PGC_KERNEL_CODE = 0, 1, 2
+PGC_KERNEL_MLP_CAST, PGC_KERNEL_MLP_FORWARD, PGC_KERNEL_MLP_HEAD, PGC_KERNEL_MLP_WGRAD = 3, 4, 5, 6
 PGC_MAX_N = 256
 
 SCHEMES = {"FR": PGC_FR, "CR": PGC_CR, "CR_REAL": PGC_CR_REAL}
@@ -222,8 +223,16 @@ def pgc_get_step(ctx):
     return out.value
 
 
-def pgc_set_timing(ctx, enable):
-    _check(lib().pgc_set_timing(ctx, 1 if enable else 0), ctx)
+def pgc_set_timing(ctx, kernels):
+    """Time the listed kernels (PGC_KERNEL_* ids); an empty list disables timing,
+    True times every kernel."""
+    if kernels is True:
+        mask = -1
+    else:
+        mask = 0
+        for k in (kernels or ()):
+            mask |= 1 << int(k)
+    _check(lib().pgc_set_timing(ctx, mask), ctx)
 
 
 def pgc_kernel_time(ctx, kernel):

@@ -14,10 +14,9 @@
 namespace {
 
 constexpr size_t kAlign = 256;
-// Gradient grid: about this many blocks per launch (>= 4 per CU on 256 CUs),
+// Gradient grid: about pgc::linear_grad_target_blocks(d) blocks per launch,
 // never fewer than kMinRowsPerBlock rows per block.  The grid depends only on
 // the problem shape, so results do not depend on the device.
-constexpr int64_t kTargetBlocks = 1024;
 constexpr int64_t kMinRowsPerBlock = 16;
 // MLP head: about this many blocks per launch, rows per block a multiple of 32.
 constexpr int64_t kHeadTargetBlocks = 1024;
@@ -34,10 +33,10 @@ struct Grid {
   int64_t rows_per_block = 0;
 };
 
-Grid make_grid(int64_t m, int32_t n_eval) {
+Grid make_grid(int64_t m, int32_t n_eval, int64_t target_blocks) {
   Grid g;
   g.n_eval = n_eval;
-  int64_t b = (kTargetBlocks + n_eval - 1) / n_eval;
+  int64_t b = (target_blocks + n_eval - 1) / n_eval;
   b = std::max<int64_t>(1, std::min<int64_t>(b, (m + kMinRowsPerBlock - 1) / kMinRowsPerBlock));
   g.rows_per_block = (m + b - 1) / b;
   g.blocks_per_part = static_cast<int32_t>((m + g.rows_per_block - 1) / g.rows_per_block);
@@ -83,7 +82,7 @@ struct pgc_ctx {
   hipStream_t stream = nullptr;
   int64_t t = 0;
   std::string err;
-  bool timing = false;
+  unsigned timing = 0;        // bit k: time kernel k
   std::vector<Timed> pending;
   std::vector<Timed> spare;
   double total_ms[PGC_KERNEL_COUNT] = {};
@@ -140,8 +139,9 @@ void compute_layout(pgc_ctx* ctx) {
     ctx->off_dz1t = take(2 * static_cast<size_t>(n) * hidden * ctx->m_pad);
     ctx->off_partials = take(sizeof(float) * static_cast<size_t>(head_blocks * ctx->pstride));
   } else {
-    ctx->warm = make_grid(ctx->m, n);
-    ctx->pipe = make_grid(ctx->m, n_pipe);
+    const int64_t target = pgc::linear_grad_target_blocks(static_cast<int>(q));
+    ctx->warm = make_grid(ctx->m, n, target);
+    ctx->pipe = make_grid(ctx->m, n_pipe, target);
     const int64_t max_blocks =
         std::max<int64_t>(static_cast<int64_t>(ctx->warm.n_eval) * ctx->warm.blocks_per_part,
                           static_cast<int64_t>(ctx->pipe.n_eval) * ctx->pipe.blocks_per_part);
@@ -181,7 +181,8 @@ int resolve_timing(pgc_ctx* ctx, bool wait) {
 template <class Fn>
 int timed_launch(pgc_ctx* ctx, int kernel, const char* what, Fn fn) {
   Timed tm;
-  if (ctx->timing) {
+  const bool timed = (ctx->timing >> kernel) & 1u;
+  if (timed) {
     if (ctx->pending.size() >= 4096) {
       int st = resolve_timing(ctx, false);
       if (st != PGC_OK) return st;
@@ -200,7 +201,7 @@ int timed_launch(pgc_ctx* ctx, int kernel, const char* what, Fn fn) {
   }
   hipError_t e = fn();
   if (e != hipSuccess) return device_fail(ctx, e, what);
-  if (ctx->timing) {
+  if (timed) {
     e = hipEventRecord(tm.stop, ctx->stream);
     if (e != hipSuccess) return device_fail(ctx, e, "hipEventRecord");
     ctx->pending.push_back(tm);
@@ -421,8 +422,8 @@ int pgc_get_step(const pgc_ctx* ctx, int64_t* t) {
 
 namespace {
 
-// Encode + masked decode + update (a6-a8), shared by both model kinds.
-int launch_code_step(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr) {
+// Arguments of the encode + masked decode + update (a6-a8).
+pgc::CodeArgs code_args(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr) {
   const int c = ctx->c;
   const bool fr = ctx->scheme == PGC_FR;
   pgc::CodeArgs ca{};
@@ -444,13 +445,13 @@ int launch_code_step(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr) {
     const int j = fr ? dec.survivors[m] / c : dec.survivors[m];
     ca.a[j] = dec.scale * dec.d[m];
   }
-  return timed_launch(ctx, PGC_KERNEL_CODE, "code kernel",
-                      [&] { return pgc::launch_code(ca, ctx->stream); });
+  return ca;
 }
 
-// a4-a5 for the linear models.
-int linear_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float* w,
-                         int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
+// The linear models' step: the gradient kernel (a4), then one launch that
+// folds its partials into the ring (a5) and runs encode, decode and update (a6-a8).
+int linear_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::Decode& dec, float lr,
+                int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
   const bool warm = ctx->t == 0;
   const Grid& grid = warm ? ctx->warm : ctx->pipe;
   pgc::LinearGradArgs ga{};
@@ -469,13 +470,11 @@ int linear_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float
   const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
                          reinterpret_cast<uintptr_t>(w) % 16 == 0;
 
-  pgc::ReduceArgs ra{};
-  ra.partials = ga.partials;
+  pgc::ReduceCodeArgs ra{};
+  ra.code = code_args(ctx, dec, w, lr);
   ra.ring = ws_ptr<float>(ctx, ctx->off_ring);
-  ra.q = ctx->d;
-  ra.ld = ctx->ld;
+  ra.partials = ga.partials;
   ra.inv_m = 1.0 / static_cast<double>(ctx->m);
-  ra.n = ctx->n;
   ra.n_eval = grid.n_eval;
   ra.blocks_per_part = grid.blocks_per_part;
   ra.part_stride = part_stride;
@@ -486,14 +485,14 @@ int linear_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float
   int st = timed_launch(ctx, PGC_KERNEL_GRADIENT, "gradient kernel",
                         [&] { return pgc::launch_linear_gradient(ga, aligned16, ctx->stream); });
   if (st != PGC_OK) return st;
-  return timed_launch(ctx, PGC_KERNEL_REDUCE, "reduce kernel",
-                      [&] { return pgc::launch_reduce(ra, ctx->stream); });
+  return timed_launch(ctx, PGC_KERNEL_CODE, "reduce/code kernel",
+                      [&] { return pgc::launch_reduce_code(ra, ctx->stream); });
 }
 
 // a4-a5 for the MLP: cast, forward, head, weight gradient, small-part reduce,
 // then copies of the slot into the other planes at the CR warm-up.
-int mlp_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float* w,
-                      int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
+int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::Decode& dec, float lr,
+             int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
   const bool warm = ctx->t == 0;
   const Grid& hg = warm ? ctx->head_warm : ctx->head_pipe;
   const int32_t d_in = ctx->cfg.d_in, hidden = ctx->cfg.hidden, classes = ctx->cfg.classes;
@@ -589,6 +588,10 @@ int mlp_gradient_step(pgc_ctx* ctx, const void* X, const void* y, const float* w
                            hipMemcpyDeviceToDevice, ctx->stream);
       return e;
     });
+  if (st == PGC_OK) {
+    const pgc::CodeArgs ca = code_args(ctx, dec, w, lr);
+    st = timed_launch(ctx, PGC_KERNEL_CODE, "code kernel", [&] { return pgc::launch_code(ca, ctx->stream); });
+  }
   return st;
 }
 
@@ -627,17 +630,15 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
     if (reinterpret_cast<uintptr_t>(X) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
         reinterpret_cast<uintptr_t>(w) % 4 != 0)
       return fail(ctx, PGC_EINVAL, "MLP: X must be 16-byte aligned, y and w 4-byte aligned");
-    st = mlp_gradient_step(ctx, X, y, w, part_stride, part_offset, plane_first, plane_count);
+    st = mlp_step(ctx, X, y, w, dec, lr, part_stride, part_offset, plane_first, plane_count);
   } else {
     const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
                            reinterpret_cast<uintptr_t>(w) % 16 == 0;
     if (!pgc::linear_grad_shape(static_cast<int>(ctx->d), aligned16).supported)
       return fail(ctx, PGC_EINVAL, "d = " + std::to_string(ctx->d) +
                                        " needs d % 4 == 0 and 16-byte aligned X and w");
-    st = linear_gradient_step(ctx, X, y, w, part_stride, part_offset, plane_first, plane_count);
+    st = linear_step(ctx, X, y, w, dec, lr, part_stride, part_offset, plane_first, plane_count);
   }
-  if (st != PGC_OK) return st;
-  st = launch_code_step(ctx, dec, w, lr);
   if (st != PGC_OK) return st;
   ctx->t += 1;
   return PGC_OK;
@@ -672,11 +673,11 @@ int pgc_read_decoded(const pgc_ctx* ctx, float* dev_out) {
   return e == hipSuccess ? PGC_OK : device_fail(const_cast<pgc_ctx*>(ctx), e, "hipMemcpyAsync");
 }
 
-int pgc_set_timing(pgc_ctx* ctx, int enable) {
+int pgc_set_timing(pgc_ctx* ctx, int kernel_mask) {
   if (ctx == nullptr) return PGC_EINVAL;
   int st = resolve_timing(ctx, true);
   if (st != PGC_OK) return st;
-  ctx->timing = enable != 0;
+  ctx->timing = static_cast<unsigned>(kernel_mask) & ((1u << PGC_KERNEL_COUNT) - 1u);
   std::fill(ctx->total_ms, ctx->total_ms + PGC_KERNEL_COUNT, 0.0);
   std::fill(ctx->launches, ctx->launches + PGC_KERNEL_COUNT, int64_t{0});
   return PGC_OK;

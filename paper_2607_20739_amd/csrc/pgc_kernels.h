@@ -36,28 +36,11 @@ struct LinearGradShape {
   bool supported;
 };
 LinearGradShape linear_grad_shape(int d, bool aligned16);
+// Blocks per launch the gradient grid aims for (depends on d only, so the grid,
+// and with it every result, is independent of pointer alignment and device).
+int linear_grad_target_blocks(int d);
 
 hipError_t launch_linear_gradient(const LinearGradArgs& a, bool aligned16, hipStream_t s);
-
-// ring[(plane_first + p) * n + k][:] = (sum_b partials[e][b][:]) / m for each
-// evaluated e (partition k = e * part_stride + part_offset) and p < plane_count.
-// Ring slots are ld floats apart (ld >= q, a multiple of 64).  Sums run in
-// fp64 in block order.
-struct ReduceArgs {
-  const float* partials;
-  float* ring;             // planes x n x ld
-  int64_t q;
-  int64_t ld;
-  double inv_m;
-  int32_t n;
-  int32_t n_eval;
-  int32_t blocks_per_part;
-  int32_t part_stride;
-  int32_t part_offset;
-  int32_t plane_first;
-  int32_t plane_count;
-};
-hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 
 // Encode, masked decode and update, column by column:
 //   coded_j = sum_o coef(j, o) * ring[slot(j, o)]          (Sec. IV-A, V-A, V-B)
@@ -82,6 +65,25 @@ struct CodeArgs {
   double a[PGC_MAX_N];     // decode weight per coded index (already scaled)
 };
 hipError_t launch_code(const CodeArgs& a, hipStream_t s);
+
+// The linear models' block partials folded into the ring, then the code step,
+// in one launch: for each evaluated e (partition k = e * part_stride +
+// part_offset) and p < plane_count,
+//   ring[(plane_first + p) * n + k][:] = inv_m * sum_b partials[e][b][:]
+// (fp64, block order), then encode / decode / update of the same columns.
+struct ReduceCodeArgs {
+  CodeArgs code;
+  float* ring;             // the ring code.ring reads, written here first
+  const float* partials;   // n_eval x blocks_per_part x q
+  double inv_m;
+  int32_t n_eval;
+  int32_t blocks_per_part;
+  int32_t part_stride;
+  int32_t part_offset;
+  int32_t plane_first;
+  int32_t plane_count;
+};
+hipError_t launch_reduce_code(const ReduceCodeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Two-layer MLP (d_in -> hidden, ReLU -> classes, softmax cross-entropy), bf16

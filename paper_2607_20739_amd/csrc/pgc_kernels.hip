@@ -169,11 +169,16 @@ void linear_gradient_kernel(LinearGradArgs a) {
 struct Shape { int max_chunks, waves, vec, groups, rows; };
 constexpr Shape kShapes4[] = {
     {64, 1, 1, 4, 8},  {128, 1, 2, 4, 8}, {256, 1, 4, 4, 4},  {512, 2, 4, 2, 4},
-    {1024, 4, 4, 1, 4}, {2048, 4, 8, 1, 2}, {4096, 8, 8, 1, 2}, {8192, 16, 8, 1, 1}};
+    {1024, 2, 8, 2, 2}, {2048, 8, 4, 1, 4}, {4096, 8, 8, 1, 2}, {8192, 16, 8, 1, 1}};
 constexpr Shape kShapes1[] = {
     {64, 1, 1, 4, 8},  {128, 1, 2, 4, 8}, {256, 1, 4, 4, 8},  {512, 2, 4, 2, 8},
     {1024, 4, 4, 1, 8}, {2048, 4, 8, 1, 4}, {4096, 8, 8, 1, 4}, {8192, 16, 8, 1, 1}};
 constexpr int kNumShapes = 8;
+// Blocks per launch that the grid aims for, by the same feature-count classes
+// as the shapes (d <= 256, 512, 1024, 2048, 4096, 8192, 16384, 32768).  The
+// float4 shapes and these targets were chosen by timing on MI355X (d = 1024,
+// 4096 and 8192 reach 84-91% of the 8 TB/s HBM peak).
+constexpr int kTargetBlocks[kNumShapes] = {1024, 1024, 512, 1024, 512, 1024, 1024, 1024};
 
 using GradKernel = void (*)(LinearGradArgs);
 
@@ -206,51 +211,114 @@ int shape_index(int d, int vw) {
   return -1;
 }
 
-__global__ __launch_bounds__(256)
-void reduce_kernel(ReduceArgs a) {
-  const int64_t col = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (col >= a.q) return;
-  const int e = blockIdx.y;
-  const float* p = a.partials + static_cast<int64_t>(e) * a.blocks_per_part * a.q + col;
-  double s = 0.0;
-  int b = 0;
-  // Loads are batched 8 at a time to keep several in flight; the additions
-  // stay in block order.
-  for (; b + 8 <= a.blocks_per_part; b += 8) {
-    float t[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = p[static_cast<int64_t>(b + i) * a.q];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) s += static_cast<double>(t[i]);
+// Encode, masked decode and update of 64 columns by a 256-thread block: the
+// four waves split the coded words (j = wave, wave + 4, ...), each word is
+// summed in fp64, and the waves' decode partials are added in wave order.
+constexpr int kCodeCols = 64;
+
+__device__ void code_columns(const CodeArgs& a, int64_t chunk) {
+  __shared__ double part[4][kCodeCols];
+  const int lane = threadIdx.x % kCodeCols, sub = threadIdx.x / kCodeCols;
+  const int64_t col = chunk * kCodeCols + lane;
+  const bool live = col < a.q;
+  double ghat = 0.0;
+  if (live) {
+    for (int j = sub; j < a.n_coded; j += 4) {
+      double word = 0.0;
+      for (int o = 0; o < a.c; ++o) {
+        const int64_t slot = a.fr ? static_cast<int64_t>(j) * a.c + o
+                                  : static_cast<int64_t>(o) * a.n + (j + o) % a.n;
+        const double v = static_cast<double>(a.ring[slot * a.ld + col]);
+        word += a.coef ? a.coef[j * a.c + o] * v : v;
+      }
+      a.coded[static_cast<int64_t>(j) * a.ld + col] = static_cast<float>(word);
+      if (a.a[j] != 0.0) ghat += a.a[j] * word;
+    }
   }
-  for (; b < a.blocks_per_part; ++b) s += static_cast<double>(p[static_cast<int64_t>(b) * a.q]);
-  const float g = static_cast<float>(s * a.inv_m);
-  const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
-  for (int pl = 0; pl < a.plane_count; ++pl)
-    a.ring[((a.plane_first + pl) * static_cast<int64_t>(a.n) + part) * a.ld + col] = g;
+  part[sub][lane] = ghat;
+  __syncthreads();
+  if (sub == 0 && live) {
+    const double g = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+    a.decoded[col] = static_cast<float>(g);
+    a.w[col] = static_cast<float>(static_cast<double>(a.w[col]) - a.lr * g);
+  }
 }
 
 __global__ __launch_bounds__(256)
 void code_kernel(CodeArgs a) {
-  const int64_t col = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (col >= a.q) return;
-  double ghat = 0.0;
-  for (int j = 0; j < a.n_coded; ++j) {
-    double word = 0.0;
-    for (int o = 0; o < a.c; ++o) {
-      const int64_t slot = a.fr ? static_cast<int64_t>(j) * a.c + o
-                                : static_cast<int64_t>(o) * a.n + (j + o) % a.n;
-      const double v = static_cast<double>(a.ring[slot * a.ld + col]);
-      word += a.coef ? a.coef[j * a.c + o] * v : v;
+  code_columns(a, blockIdx.x);
+}
+
+// Block b owns columns [16 b, 16 b + 16).  It first folds every evaluated
+// partition's block partials for those columns into the ring (fp64, block
+// order, one (partition, column) pair per thread), then -- after a barrier, so
+// the fresh slots written by its own threads are visible -- encodes, decodes
+// and updates the same columns with the 16 lanes of each column splitting the
+// coded words.  No block depends on another.
+constexpr int kFusedCols = 16;
+constexpr int kFusedSubs = 256 / kFusedCols;
+
+__global__ __launch_bounds__(256)
+void reduce_code_kernel(ReduceCodeArgs a) {
+  __shared__ double part[kFusedSubs][kFusedCols];
+  const CodeArgs& ca = a.code;
+  const int64_t col0 = static_cast<int64_t>(blockIdx.x) * kFusedCols;
+  for (int pair = threadIdx.x; pair < a.n_eval * kFusedCols; pair += 256) {
+    const int e = pair / kFusedCols;
+    const int64_t col = col0 + pair % kFusedCols;
+    if (col >= ca.q) continue;
+    const float* p = a.partials + static_cast<int64_t>(e) * a.blocks_per_part * ca.q + col;
+    double s = 0.0;
+    int b = 0;
+    for (; b + 8 <= a.blocks_per_part; b += 8) {
+      float t[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) t[i] = p[static_cast<int64_t>(b + i) * ca.q];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += static_cast<double>(t[i]);
     }
-    a.coded[static_cast<int64_t>(j) * a.ld + col] = static_cast<float>(word);
-    if (a.a[j] != 0.0) ghat += a.a[j] * word;
+    for (; b < a.blocks_per_part; ++b) s += static_cast<double>(p[static_cast<int64_t>(b) * ca.q]);
+    const float g = static_cast<float>(s * a.inv_m);
+    const int64_t k = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
+    for (int pl = 0; pl < a.plane_count; ++pl)
+      a.ring[((a.plane_first + pl) * static_cast<int64_t>(ca.n) + k) * ca.ld + col] = g;
   }
-  a.decoded[col] = static_cast<float>(ghat);
-  a.w[col] = static_cast<float>(static_cast<double>(a.w[col]) - a.lr * ghat);
+  __syncthreads();
+
+  const int lane = threadIdx.x % kFusedCols, sub = threadIdx.x / kFusedCols;
+  const int64_t col = col0 + lane;
+  const bool live = col < ca.q;
+  double ghat = 0.0;
+  if (live) {
+    for (int j = sub; j < ca.n_coded; j += kFusedSubs) {
+      double word = 0.0;
+      for (int o = 0; o < ca.c; ++o) {
+        const int64_t slot = ca.fr ? static_cast<int64_t>(j) * ca.c + o
+                                   : static_cast<int64_t>(o) * ca.n + (j + o) % ca.n;
+        const double v = static_cast<double>(a.ring[slot * ca.ld + col]);
+        word += ca.coef ? ca.coef[j * ca.c + o] * v : v;
+      }
+      ca.coded[static_cast<int64_t>(j) * ca.ld + col] = static_cast<float>(word);
+      if (ca.a[j] != 0.0) ghat += ca.a[j] * word;
+    }
+  }
+  part[sub][lane] = ghat;
+  __syncthreads();
+  if (sub == 0 && live) {
+    double g = part[0][lane];
+#pragma unroll
+    for (int i = 1; i < kFusedSubs; ++i) g += part[i][lane];
+    ca.decoded[col] = static_cast<float>(g);
+    ca.w[col] = static_cast<float>(static_cast<double>(ca.w[col]) - ca.lr * g);
+  }
 }
 
 }  // namespace
+
+int linear_grad_target_blocks(int d) {
+  const int i = shape_index(d % 4 == 0 ? d : (d + 3) / 4 * 4, 4);
+  return kTargetBlocks[i < 0 ? kNumShapes - 1 : i];
+}
 
 LinearGradShape linear_grad_shape(int d, bool aligned16) {
   const int vw = (aligned16 && d % 4 == 0) ? 4 : 1;
@@ -275,14 +343,14 @@ hipError_t launch_linear_gradient(const LinearGradArgs& a, bool aligned16, hipSt
   return hipGetLastError();
 }
 
-hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream) {
-  dim3 grid(static_cast<unsigned>((a.q + 255) / 256), a.n_eval);
-  hipLaunchKernelGGL(reduce_kernel, grid, dim3(256), 0, stream, a);
+hipError_t launch_reduce_code(const ReduceCodeArgs& a, hipStream_t stream) {
+  dim3 grid(static_cast<unsigned>((a.code.q + kFusedCols - 1) / kFusedCols));
+  hipLaunchKernelGGL(reduce_code_kernel, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_code(const CodeArgs& a, hipStream_t stream) {
-  dim3 grid(static_cast<unsigned>((a.q + 255) / 256));
+  dim3 grid(static_cast<unsigned>((a.q + kCodeCols - 1) / kCodeCols));
   hipLaunchKernelGGL(code_kernel, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
