@@ -28,15 +28,17 @@ HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 DEFAULT_WORKLOAD = "crreal_lsq_n8_c3_d1024"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_kernels.hip")
+KERNEL_SOURCES = {"hbm": os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_linear.hip"),
+                  "mfma": os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_mlp.hip")}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
+def kernel_source_hash(bound):
+    """Hash of the source file that holds the dominant kernel of a workload."""
+    with open(KERNEL_SOURCES[bound], "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
@@ -73,16 +75,16 @@ def mlp_gemm_flops(w):
     return 2.0 * rows_per_step(w) * w.d * w.hidden
 
 
-def read_traffic(workload):
-    """HBM bytes per gradient launch measured by rocprofv3 counters, if they were
-    taken on the current kernel source; else None."""
+def read_traffic(workload, bound):
+    """HBM bytes per launch of the dominant kernel measured by rocprofv3 counters,
+    if they were taken on the current kernel source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             data = json.load(f)
     except (OSError, ValueError):
         return None
     entry = data.get(workload)
-    if not entry or entry.get("kernel_source_sha256_16") != kernel_source_hash():
+    if not entry or entry.get("kernel_source_sha256_16") != kernel_source_hash(bound):
         return None
     return entry.get("bytes_per_launch")
 
@@ -107,10 +109,10 @@ def cpu_baseline(w, X, y, beta0, budget_s):
               keep_coded=False, keep_alpha=False)
         return time.perf_counter() - t0
 
-    t2, t6 = run(2), run(6)
-    per_step = max((t6 - t2) / 4, 1e-6)
-    fixed = max(t2 - 2 * per_step, 0.0)
-    steps = int(max(2, min(max_steps, (budget_s - fixed) / per_step)))
+    # Size the sample from a 6-step probe (whose time includes the one-time
+    # setup, so the estimate errs on the short side).
+    per_step = max(run(6) / 6, 1e-6)
+    steps = int(max(2, min(max_steps, budget_s / per_step)))
     elapsed = run(steps)
     threads = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
     cores = min(max(threads) if threads else 1, len(os.sched_getaffinity(0)))
@@ -216,12 +218,12 @@ def main():
         achieved = mlp_gemm_flops(w) / (per_launch[dominant] * 1e-3) / 1e12
         roofline = {"bound": "mfma", "kernel": dominant, "achieved": achieved,
                     "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": read_traffic(w.name)}
+                    "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": read_traffic(w.name, "mfma")}
     else:
         achieved = grad_bytes / (per_launch["gradient"] * 1e-3) / 1e9
         roofline = {"bound": "hbm", "kernel": "linear_gradient_kernel", "achieved": achieved,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                    "traffic": read_traffic(w.name)}
+                    "traffic": read_traffic(w.name, "hbm")}
     log("step %.4f ms; per launch (ms): %s" % (ms_per_step, ", ".join(
         "%s %.4f" % kv for kv in per_launch.items())))
 
