@@ -9,42 +9,49 @@
 namespace pgc {
 namespace {
 
-// Encode, masked decode and update of 64 columns by a 256-thread block: the
-// four waves split the coded words (j = wave, wave + 4, ...), each word is
-// summed in fp64, and the waves' decode partials are added in wave order.
-constexpr int kCodeCols = 64;
-
-__device__ void code_columns(const CodeArgs& a, int64_t chunk) {
-  __shared__ double part[4][kCodeCols];
-  const int lane = threadIdx.x % kCodeCols, sub = threadIdx.x / kCodeCols;
-  const int64_t col = chunk * kCodeCols + lane;
-  const bool live = col < a.q;
-  double ghat = 0.0;
-  if (live) {
-    for (int j = sub; j < a.n_coded; j += 4) {
-      double word = 0.0;
-      for (int o = 0; o < a.c; ++o) {
-        const int64_t slot = a.fr ? static_cast<int64_t>(j) * a.c + o
-                                  : static_cast<int64_t>(o) * a.n + (j + o) % a.n;
-        const double v = static_cast<double>(a.ring[slot * a.ld + col]);
-        word += a.coef ? a.coef[j * a.c + o] * v : v;
-      }
-      a.coded[static_cast<int64_t>(j) * a.ld + col] = static_cast<float>(word);
-      if (a.a[j] != 0.0) ghat += a.a[j] * word;
-    }
-  }
-  part[sub][lane] = ghat;
-  __syncthreads();
-  if (sub == 0 && live) {
-    const double g = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
-    a.decoded[col] = static_cast<float>(g);
-    a.w[col] = static_cast<float>(static_cast<double>(a.w[col]) - a.lr * g);
-  }
-}
+// Encode, masked decode and update of 256 columns by a 256-thread block: a
+// thread owns 4 consecutive columns (16-byte ring loads; slots are padded to
+// ld, a multiple of 256, so a block never leaves its slot), the four waves split
+// the coded words (j = wave, wave + 4, ...), each word is summed in fp64, and
+// the waves' decode partials are added in wave order.
+constexpr int kCodeCols = 256;
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256)
 void code_kernel(CodeArgs a) {
-  code_columns(a, blockIdx.x);
+  __shared__ double part[4][kCodeCols];
+  const int lane = threadIdx.x % 64, sub = threadIdx.x / 64;
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * kCodeCols + 4 * lane;
+  double ghat[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int j = sub; j < a.n_coded; j += 4) {
+    double word[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int o = 0; o < a.c; ++o) {
+      const int64_t slot = a.fr ? static_cast<int64_t>(j) * a.c + o
+                                : static_cast<int64_t>(o) * a.n + (j + o) % a.n;
+      const f4v v = *reinterpret_cast<const f4v*>(a.ring + slot * a.ld + col);
+      const double cf = a.coef ? a.coef[j * a.c + o] : 1.0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) word[i] += cf * static_cast<double>(v[i]);
+    }
+    f4v out;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = static_cast<float>(word[i]);
+    *reinterpret_cast<f4v*>(a.coded + static_cast<int64_t>(j) * a.ld + col) = out;
+    if (a.a[j] != 0.0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ghat[i] += a.a[j] * word[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) part[sub][4 * lane + i] = ghat[i];
+  __syncthreads();
+  const int c = threadIdx.x;   // one column per thread for the result
+  const int64_t gc = static_cast<int64_t>(blockIdx.x) * kCodeCols + c;
+  if (gc < a.q) {
+    const double g = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
+    a.decoded[gc] = static_cast<float>(g);
+    a.w[gc] = static_cast<float>(static_cast<double>(a.w[gc]) - a.lr * g);
+  }
 }
 
 // Block b owns columns [16 b, 16 b + 16).  It first folds every evaluated

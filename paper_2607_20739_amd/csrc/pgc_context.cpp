@@ -18,11 +18,12 @@ constexpr size_t kAlign = 256;
 // never fewer than kMinRowsPerBlock rows per block.  The grid depends only on
 // the problem shape, so results do not depend on the device.
 constexpr int64_t kMinRowsPerBlock = 16;
-// MLP head: about this many blocks per launch, rows per block a multiple of 32.
+// MLP head: about this many blocks per launch, rows per block a multiple of 64.
 constexpr int64_t kHeadTargetBlocks = 1024;
-// Ring slots and coded words are padded to a multiple of this many floats so
-// every slot starts 256-byte aligned.
-constexpr int64_t kSlotAlign = 64;
+// Ring slots and coded words are padded to a multiple of this many floats:
+// every slot starts 1 KiB aligned, and the code kernel's 256-column blocks
+// cover a slot exactly (never spilling into the next one).
+constexpr int64_t kSlotAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
@@ -43,13 +44,13 @@ Grid make_grid(int64_t m, int32_t n_eval, int64_t target_blocks) {
   return g;
 }
 
-// Head grid of the MLP: blocks of a multiple of 32 rows over the m_pad rows.
+// Head grid of the MLP: blocks of a multiple of 64 rows over the m_pad rows.
 Grid make_head_grid(int64_t m_pad, int32_t n_eval) {
   Grid g;
   g.n_eval = n_eval;
   int64_t b = (kHeadTargetBlocks + n_eval - 1) / n_eval;
-  b = std::max<int64_t>(1, std::min<int64_t>(b, m_pad / 32));
-  g.rows_per_block = round_up((m_pad + b - 1) / b, 32);
+  b = std::max<int64_t>(1, std::min<int64_t>(b, m_pad / 64));
+  g.rows_per_block = round_up((m_pad + b - 1) / b, 64);
   g.blocks_per_part = static_cast<int32_t>((m_pad + g.rows_per_block - 1) / g.rows_per_block);
   return g;
 }
@@ -124,8 +125,8 @@ void compute_layout(pgc_ctx* ctx) {
   ctx->off_coef = take(sizeof(double) * ctx->coef.size());
   if (ctx->cfg.model == PGC_MLP) {
     const int64_t hidden = ctx->cfg.hidden;
-    ctx->kpad = round_up(ctx->cfg.d_in, 32);
-    ctx->m_pad = round_up(ctx->m, 32);
+    ctx->kpad = round_up(ctx->cfg.d_in, 64);   // the forward GEMM's K step
+    ctx->m_pad = round_up(ctx->m, 64);   // the weight-gradient GEMM's K step
     ctx->pstride = (pgc::kMlpMaxClasses + 1) * hidden + pgc::kMlpMaxClasses;
     ctx->head_warm = make_head_grid(ctx->m_pad, n);
     ctx->head_pipe = make_head_grid(ctx->m_pad, n_pipe);

@@ -50,7 +50,7 @@ hipError_t launch_linear_gradient(const LinearGradArgs& a, bool aligned16, hipSt
 // CR: j is a worker, slot(j, o) = plane o, partition (j + o) mod n.
 // coef == nullptr means unit coefficients; else coef[j * c + o] (fp64).
 struct CodeArgs {
-  const float* ring;       // planes x n x ld
+  const float* ring;       // planes x n x ld  (ld >= q, a multiple of 256)
   float* coded;            // n_coded x ld
   float* decoded;          // q
   float* w;                // q
@@ -95,7 +95,8 @@ hipError_t launch_reduce_code(const ReduceCodeArgs& a, hipStream_t s);
 constexpr int kMlpMaxClasses = 16;
 constexpr int kMlpMaxHidden = 1024;
 
-// bf16 copies of the weights for the GEMMs: W1T[hidden][kpad] (zero past d_in),
+// bf16 copies of the weights for the GEMMs: W1T[hidden][kpad] (kpad a multiple
+// of 64; zero past d_in),
 // W2T[16][hidden] and W2p[hidden][16] (zero past `classes`).
 struct MlpCastArgs {
   const float* w;
@@ -119,8 +120,8 @@ struct MlpForwardArgs {
 hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s);
 
 // Per 16-row tile: logits, softmax, dZ2 = (p - onehot(y)) / m, dZ1 = (dZ2 W2^T)
-// masked by H > 0, written transposed to dZ1T[e][h][r] (r < m_pad, zero for
-// r >= m).  Each block writes partial sums of dW2^T[16][hidden], db1[hidden]
+// masked by H > 0, written transposed to dZ1T[e][h][r] (r < m_pad, a multiple
+// of 64; zero for r >= m).  Each block writes partial sums of dW2^T[16][hidden], db1[hidden]
 // and db2[16] to partials[(e * blocks_per_part + b) * pstride].
 struct MlpHeadArgs {
   const __bf16* H;

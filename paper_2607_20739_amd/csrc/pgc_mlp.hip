@@ -4,7 +4,8 @@
 //
 // Per step, for the evaluated partitions:
 //   cast     w (fp32) -> W1T, W2T, W2p (bf16 copies laid out for the MFMAs)
-//   forward  H = relu(X W1 + b1)                       MFMA 16x16x32, LDS-tiled
+//   forward  H = relu(X W1 + b1)                       MFMA 16x16x32, LDS-tiled,
+//            register prefetch, XCD-aware tile order
 //   head     logits = H W2 + b2, softmax, dZ2 = (p - onehot) / m,
 //            dZ1 = (dZ2 W2^T) * [H > 0] (stored transposed), and block
 //            partials of dW2 = H^T dZ2, db1, db2         MFMA 16x16x32 / 16x16x16
@@ -69,86 +70,104 @@ void mlp_cast_w2_kernel(MlpCastArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// forward: H = relu(X W1 + b1), block tile 128 rows x 256 hidden, K step 32,
-// 4 waves as 2 x 2 (64 x 128 each), double-buffered LDS.
+// forward: H = relu(X W1 + b1).  Block tile 128 rows x 128 hidden, K step 64,
+// 4 waves as 2 x 2 (64 x 64 each) on 16x16x32 MFMAs, two blocks per CU.
+// Global tiles are fetched one K step ahead into registers and staged
+// through double-buffered LDS (one barrier per K step).  Block ids are mapped
+// so that all hidden tiles of a row tile run on the same XCD (workgroups are
+// dealt to the 8 XCDs round-robin) and share that XCD's L2 copy of X.
 // ---------------------------------------------------------------------------
 
-constexpr int kFwBM = 128, kFwBN = 256, kFwBK = 32, kFwLd = kFwBK + 8;
+constexpr int kFwBM = 128, kFwBN = 128, kFwBK = 64, kFwLd = kFwBK + 8;
+constexpr int kXcds = 8;
 
-__global__ __launch_bounds__(256)
+struct FwStage {
+  bf16x8 a[4], b[4];
+};
+
+__global__ __launch_bounds__(256, 2)
 void mlp_forward_kernel(MlpForwardArgs a) {
   __shared__ bf16 As[2][kFwBM][kFwLd];
   __shared__ bf16 Bs[2][kFwBN][kFwLd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
-  const int h0 = blockIdx.x * kFwBN;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kFwBM;
-  const int e = blockIdx.z;
+
+  const int htiles = a.hidden / kFwBN;
+  const int64_t tiles_per_part = (a.m + kFwBM - 1) / kFwBM;
+  const int64_t rtiles = tiles_per_part * a.n_eval;
+  const int64_t id = blockIdx.x;
+  const int64_t rest = id / kXcds;
+  const int ht = static_cast<int>(rest % htiles);
+  const int64_t rt = (rest / htiles) * kXcds + id % kXcds;
+  if (rt >= rtiles) return;
+  const int e = static_cast<int>(rt / tiles_per_part);
+  const int64_t r0 = (rt % tiles_per_part) * kFwBM;
+  const int h0 = ht * kFwBN;
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
   const bf16* Xp = a.X + part * a.m * a.d_in;
   const int ksteps = a.kpad / kFwBK;
   const int dchunks = a.d_in / 8;
 
-  bf16x8 ra[2], rb[4];
-  auto fetch = [&](int ks) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = tid + u * 256, row = idx >> 2, ch = idx & 3;
-      const int kc = ks * 4 + ch;
-      const int64_t gr = r0 + row;
-      ra[u] = (gr < a.m && kc < dchunks) ? load_vec<bf16x8>(Xp + gr * a.d_in + kc * 8) : bf16x8{};
-    }
+  auto fetch = [&](FwStage& st, int ks) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int idx = tid + u * 256, row = idx >> 2, ch = idx & 3;
-      rb[u] = load_vec<bf16x8>(a.W1T + static_cast<int64_t>(h0 + row) * a.kpad + ks * kFwBK + ch * 8);
+      const int idx = tid + u * 256, row = idx >> 3, ch = idx & 7;
+      const int kc = ks * 8 + ch;
+      const int64_t gr = r0 + row;
+      st.a[u] = (gr < a.m && kc < dchunks) ? load_vec<bf16x8>(Xp + gr * a.d_in + kc * 8) : bf16x8{};
+      st.b[u] = load_vec<bf16x8>(a.W1T + static_cast<int64_t>(h0 + row) * a.kpad + ks * kFwBK + ch * 8);
     }
   };
-  auto stage = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = tid + u * 256;
-      *reinterpret_cast<bf16x8*>(&As[buf][idx >> 2][(idx & 3) * 8]) = ra[u];
-    }
+  auto stage = [&](const FwStage& st, int buf) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int idx = tid + u * 256;
-      *reinterpret_cast<bf16x8*>(&Bs[buf][idx >> 2][(idx & 3) * 8]) = rb[u];
+      const int idx = tid + u * 256, row = idx >> 3, ch = idx & 7;
+      *reinterpret_cast<bf16x8*>(&As[buf][row][ch * 8]) = st.a[u];
+      *reinterpret_cast<bf16x8*>(&Bs[buf][row][ch * 8]) = st.b[u];
     }
   };
 
-  f32x4 acc[4][8];
+  f32x4 acc[4][4];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = f32x4{};
+    for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x4{};
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < kFwBK / 32; ++kk) {
+      bf16x8 af[4], bfr[4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+        af[mt] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * 64 + mt * 16 + lr][kk * 32 + lg * 8]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+        bfr[nt] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * 64 + nt * 16 + lr][kk * 32 + lg * 8]);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma_k32(af[mt], bfr[nt], acc[mt][nt]);
+    }
+  };
 
-  fetch(0);
-  stage(0);
+  // Invariant at the top of step ks: LDS buffer ks % 2 holds step ks and the
+  // registers s0 hold step ks + 1.
+  FwStage s0;
+  fetch(s0, 0);
+  stage(s0, 0);
   __syncthreads();
+  if (1 < ksteps) fetch(s0, 1);
   for (int ks = 0; ks < ksteps; ++ks) {
-    const int buf = ks & 1;
-    if (ks + 1 < ksteps) fetch(ks + 1);
-    bf16x8 af[4], bfr[8];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-      af[mt] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * 64 + mt * 16 + lr][lg * 8]);
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt)
-      bfr[nt] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * 128 + nt * 16 + lr][lg * 8]);
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = mfma_k32(af[mt], bfr[nt], acc[mt][nt]);
-    if (ks + 1 < ksteps) stage(buf ^ 1);
+    compute(ks & 1);
+    if (ks + 1 < ksteps) stage(s0, (ks + 1) & 1);
     __syncthreads();
+    if (ks + 2 < ksteps) fetch(s0, ks + 2);
   }
 
   bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * a.hidden;
 #pragma unroll
-  for (int nt = 0; nt < 8; ++nt) {
-    const int h = h0 + wn * 128 + nt * 16 + lr;
+  for (int nt = 0; nt < 4; ++nt) {
+    const int h = h0 + wn * 64 + nt * 16 + lr;
     const float bias = a.b1[h];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
@@ -161,17 +180,24 @@ void mlp_forward_kernel(MlpForwardArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// head: one wave per 128 hidden columns, 16-row tiles; the wave's partial
-// logits are summed across waves through LDS in wave order.
+// head: one wave per 128 hidden columns, 16-row tiles.  The wave's partial
+// logits are summed across waves through LDS in wave order (one barrier per
+// tile).  Each wave stages its 16 x 128 tile of H and of dZ1 through its own
+// LDS area: the ReLU mask and the dW2 operand are read from there, and dZ1^T
+// leaves in 16-byte row-contiguous stores.
 // ---------------------------------------------------------------------------
 
 constexpr int kHeadCols = 128;
 constexpr int kHeadMaxWaves = kMlpMaxHidden / kHeadCols;
+constexpr int kHtLd = kHeadCols + 8;   // H tile row stride (bf16)
+constexpr int kZtLd = 16 + 8;          // dZ1^T tile row stride (bf16)
 
 __global__ __launch_bounds__(64 * kHeadMaxWaves)
 void mlp_head_kernel(MlpHeadArgs a) {
   __shared__ float zpart[2][kHeadMaxWaves][16][16];
   __shared__ float dzt[kHeadMaxWaves][16][17];
+  __shared__ bf16 Ht[kHeadMaxWaves][16][kHtLd];
+  __shared__ bf16 Zt[kHeadMaxWaves][kHeadCols][kZtLd];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int waves = a.hidden / kHeadCols;
@@ -203,16 +229,24 @@ void mlp_head_kernel(MlpHeadArgs a) {
   }
   float db2 = 0.0f;
   int buf = 0;
+  // H fragments of the logits GEMM (row r0 + lr, columns hw0 + 32 ks + 8 lg ..),
+  // fetched one tile ahead.
+  bf16x8 hnext[4];
+  auto fetch_h = [&](int64_t r0) {
+    const int64_t row = r0 + lr;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      hnext[ks] = row < a.m ? load_vec<bf16x8>(Hp + row * hidden + hw0 + ks * 32 + lg * 8) : bf16x8{};
+  };
+  if (rbeg < rend) fetch_h(rbeg);
   for (int64_t r0 = rbeg; r0 < rend; r0 += 16) {
-    // Partial logits of rows r0..r0+15 over this wave's hidden columns.
-    const int64_t row_l = r0 + lr;
-    const bool valid_l = row_l < a.m;
     f32x4 z = f32x4{};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const bf16x8 hv = valid_l ? load_vec<bf16x8>(Hp + row_l * hidden + hw0 + ks * 32 + lg * 8) : bf16x8{};
-      z = mfma_k32(hv, w2t[ks], z);
+      z = mfma_k32(hnext[ks], w2t[ks], z);
+      *reinterpret_cast<bf16x8*>(&Ht[wave][lr][ks * 32 + lg * 8]) = hnext[ks];
     }
+    if (r0 + 16 < rend) fetch_h(r0 + 16);
 #pragma unroll
     for (int i = 0; i < 4; ++i) zpart[buf][wave][lg * 4 + i][lr] = z[i];
     __syncthreads();
@@ -237,9 +271,10 @@ void mlp_head_kernel(MlpHeadArgs a) {
       db2 += dz2[i];
     }
     buf ^= 1;
+    // The transposes below go through this wave's private LDS areas; a wave's
+    // LDS operations complete in order, so they need no barrier.
 #pragma unroll
     for (int i = 0; i < 4; ++i) dzt[wave][lg * 4 + i][lr] = dz2[i];
-    __syncthreads();
     bf16x4 dz_b, dz_a;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -248,24 +283,28 @@ void mlp_head_kernel(MlpHeadArgs a) {
     }
 #pragma unroll
     for (int ht = 0; ht < 8; ++ht) {
-      const int h = hw0 + ht * 16;
+      const int h = ht * 16;   // within the wave's columns
       // dH^T[h + 4 lg + i][r0 + lr] = sum_c W2[h + 4 lg + i][c] dZ2[r0 + lr][c]
       const f32x4 dh = mfma_k16(w2p[ht], dz_b, f32x4{});
-      const bf16x4 hm = valid_l ? load_vec<bf16x4>(Hp + row_l * hidden + h + lg * 4) : bf16x4{};
+      const bf16x4 hm = *reinterpret_cast<const bf16x4*>(&Ht[wave][lr][h + lg * 4]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float g = static_cast<float>(hm[i]) > 0.0f ? dh[i] : 0.0f;
         db1[ht][i] += g;
-        dz1[(h + lg * 4 + i) * a.m_pad + row_l] = static_cast<bf16>(g);
+        Zt[wave][h + lg * 4 + i][lr] = static_cast<bf16>(g);
       }
       // dW2^T[4 lg + i][h + lr] += sum_r dZ2[r][4 lg + i] H[r][h + lr]
       bf16x4 hb;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t rr = r0 + lg * 4 + j;
-        hb[j] = rr < a.m ? Hp[rr * hidden + h + lr] : static_cast<bf16>(0.0f);
-      }
+      for (int j = 0; j < 4; ++j) hb[j] = Ht[wave][lg * 4 + j][h + lr];
       dw2[ht] = mfma_k16(dz_a, hb, dw2[ht]);
+    }
+    // dZ1^T rows: lane writes 8 consecutive rows of column hw0 + lane/2 + 32 k.
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int hl = lane / 2 + 32 * k, half = lane & 1;
+      *reinterpret_cast<bf16x8*>(dz1 + static_cast<int64_t>(hw0 + hl) * a.m_pad + r0 + half * 8) =
+          *reinterpret_cast<const bf16x8*>(&Zt[wave][hl][half * 8]);
     }
   }
 
@@ -292,11 +331,17 @@ void mlp_head_kernel(MlpHeadArgs a) {
 
 // ---------------------------------------------------------------------------
 // wgrad: dW1^T tile 256 hidden x 112 features per block, K = rows in steps of
-// 32; 4 waves, each 64 hidden x 112 features.  dZ1T rows feed the A operand
-// straight from global memory; the X tile is transposed into LDS.
+// 64; 4 waves, each 64 hidden x 112 features.  dZ1T rows feed the A operand
+// straight from global memory; the X tile is transposed into LDS as 32-bit
+// words holding two consecutive rows of one feature.  The staging lanes of a
+// wave cover 32 row pairs x 2 feature chunks, so with a row stride of 36
+// words each of its stores touches 64 distinct banks, and the B-operand reads
+// (16 rows x 16 bytes) are conflict-free as well.
 // ---------------------------------------------------------------------------
 
-constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 32, kWgLd = kWgBK + 8;
+constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 64, kWgLd = kWgBK + 8;
+constexpr int kWgPairs = kWgBK / 2;                   // row pairs per K step
+constexpr int kWgItems = kWgPairs * (kWgBN / 8);      // (row pair, feature chunk) items
 
 __global__ __launch_bounds__(256)
 void mlp_wgrad_kernel(MlpWgradArgs a) {
@@ -312,33 +357,46 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   const int ksteps = static_cast<int>(a.m_pad / kWgBK);
   const int dchunks = a.d_in / 8;
 
-  // X staging: thread t < 224 moves rows (2 rp, 2 rp + 1) x features fc*8..+7.
-  const bool stager = tid < (kWgBK / 2) * (kWgBN / 8);
-  const int rp = tid / (kWgBN / 8), fc = tid % (kWgBN / 8);
-  const bool fvalid = stager && (i0 / 8 + fc) < dchunks;
-  bf16x8 x0 = bf16x8{}, x1 = bf16x8{};
+  // Staging items t and t + 256: row pair rp = item % 32, feature chunk fc = item / 32.
+  bf16x8 x[2][2];
   auto fetch_x = [&](int ks) {
-    if (!fvalid) return;
-    const int64_t r = static_cast<int64_t>(ks) * kWgBK + 2 * rp;
-    x0 = r < a.m ? load_vec<bf16x8>(Xp + r * a.d_in + i0 + fc * 8) : bf16x8{};
-    x1 = r + 1 < a.m ? load_vec<bf16x8>(Xp + (r + 1) * a.d_in + i0 + fc * 8) : bf16x8{};
-  };
-  auto stage_x = [&](int buf) {
-    if (!stager) return;
 #pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
-      bf16x2 pair;
-      pair[0] = x0[f];
-      pair[1] = x1[f];
-      *reinterpret_cast<bf16x2*>(&XT[buf][fc * 8 + f][2 * rp]) = pair;
+    for (int u = 0; u < 2; ++u) {
+      const int item = tid + u * 256;
+      x[u][0] = bf16x8{};
+      x[u][1] = bf16x8{};
+      if (item >= kWgItems) continue;
+      const int rp = item % kWgPairs, fc = item / kWgPairs;
+      if (i0 / 8 + fc >= dchunks) continue;
+      const int64_t r = static_cast<int64_t>(ks) * kWgBK + 2 * rp;
+      if (r < a.m) x[u][0] = load_vec<bf16x8>(Xp + r * a.d_in + i0 + fc * 8);
+      if (r + 1 < a.m) x[u][1] = load_vec<bf16x8>(Xp + (r + 1) * a.d_in + i0 + fc * 8);
     }
   };
-  bf16x8 av[4];
+  auto stage_x = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int item = tid + u * 256;
+      if (item >= kWgItems) continue;
+      const int rp = item % kWgPairs, fc = item / kWgPairs;
+#pragma unroll
+      for (int f = 0; f < 8; ++f) {
+        typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        bf16x2 pair;
+        pair[0] = x[u][0][f];
+        pair[1] = x[u][1][f];
+        *reinterpret_cast<bf16x2*>(&XT[buf][fc * 8 + f][2 * rp]) = pair;
+      }
+    }
+  };
+  bf16x8 av[4][2];
   auto fetch_a = [&](int ks) {
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
-      av[mt] = load_vec<bf16x8>(dz + static_cast<int64_t>(hb0 + mt * 16 + lr) * a.m_pad + ks * kWgBK + lg * 8);
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        av[mt][kk] = load_vec<bf16x8>(dz + static_cast<int64_t>(hb0 + mt * 16 + lr) * a.m_pad +
+                                      ks * kWgBK + kk * 32 + lg * 8);
   };
 
   f32x4 acc[4][7];
@@ -353,19 +411,24 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   __syncthreads();
   for (int ks = 0; ks < ksteps; ++ks) {
     const int buf = ks & 1;
-    bf16x8 af[4];
+    bf16x8 af[4][2];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) af[mt] = av[mt];
+    for (int mt = 0; mt < 4; ++mt) {
+      af[mt][0] = av[mt][0];
+      af[mt][1] = av[mt][1];
+    }
     if (ks + 1 < ksteps) {
       fetch_x(ks + 1);
       fetch_a(ks + 1);
     }
 #pragma unroll
-    for (int nt = 0; nt < 7; ++nt) {
-      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&XT[buf][nt * 16 + lr][lg * 8]);
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt], bv, acc[mt][nt]);
-    }
+      for (int nt = 0; nt < 7; ++nt) {
+        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&XT[buf][nt * 16 + lr][kk * 32 + lg * 8]);
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt][kk], bv, acc[mt][nt]);
+      }
     if (ks + 1 < ksteps) stage_x(buf ^ 1);
     __syncthreads();
   }
@@ -421,7 +484,8 @@ hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s) {
-  dim3 grid(a.hidden / kFwBN, static_cast<unsigned>((a.m + kFwBM - 1) / kFwBM), a.n_eval);
+  const int64_t rtiles = (a.m + kFwBM - 1) / kFwBM * a.n_eval;
+  dim3 grid(static_cast<unsigned>((rtiles + kXcds - 1) / kXcds * kXcds * (a.hidden / kFwBN)));
   hipLaunchKernelGGL(mlp_forward_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
