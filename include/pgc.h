@@ -39,7 +39,8 @@ typedef struct pgc_ctx pgc_ctx;
 enum pgc_scheme {
   PGC_FR = 0,      /* PGC-FR, Sec. IV-A: groups of c workers share c partitions; needs c | n */
   PGC_CR = 1,      /* PGC-CR, Sec. V-B: cyclic placement, unit coefficients, scale 1/(|J| c) */
-  PGC_CR_REAL = 2  /* naive pipelined CR, Sec. V-A: real coefficients, exact-sum decode */
+  PGC_CR_REAL = 2, /* naive pipelined CR, Sec. V-A: real coefficients, exact-sum decode */
+  PGC_IS_SGD = 3   /* ignore-straggler SGD, Sec. VI-A: c = 1, mean of the survivors' gradients */
 };
 
 /* Model whose per-partition gradient is evaluated. */
@@ -96,7 +97,8 @@ typedef struct pgc_config {
 
 /* Create a context for `scheme` with n workers (= partitions), c partitions per
  * worker (s = c - 1 tolerated stragglers) and a parameter vector of length d.
- * Requires 1 <= c <= n <= PGC_MAX_N, d >= 1, and c | n for PGC_FR.
+ * Requires 1 <= c <= n <= PGC_MAX_N, d >= 1, c | n for PGC_FR and c = 1 for
+ * PGC_IS_SGD (which ignores up to n - 1 stragglers).
  * Sec. III (placements), Sec. IV-A, Sec. V-A, Sec. V-B.  Touches no GPU.
  * *out receives the handle (NULL on failure; reason via pgc_strerror). */
 int pgc_init(pgc_ctx** out, int scheme, int n, int c, int64_t d);
@@ -108,6 +110,14 @@ int pgc_init(pgc_ctx** out, int scheme, int n, int c, int64_t d);
  * code_seed (PGC_ESINGULAR if a row's defining system is singular).
  * Resets the step counter to 0 and invalidates a bound workspace.  Host only. */
 int pgc_configure(pgc_ctx* ctx, const pgc_config* cfg);
+
+/* Pipelining on (1, the default: PGC) or off (0: gradient coding).  With it
+ * off every step evaluates all c partitions each worker holds at the current
+ * w, as the warm-up step does, so the coded gradients are current (GC,
+ * Sec. III / IV-A); with FR or PGC_CR_REAL the decode then recovers the full
+ * gradient exactly and the run coincides with distributed gradient descent.
+ * Takes effect from the next pgc_step.  Host only. */
+int pgc_set_pipelining(pgc_ctx* ctx, int enabled);
 
 /* Stream (a hipStream_t, NULL = the null stream) on which pgc_step and the
  * pgc_read_* calls enqueue work.  Default: the null stream. */
@@ -139,7 +149,8 @@ int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes);
 int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
              const uint8_t* straggler_mask, float lr);
 
-/* Decode coefficients of `straggler_mask` (host, n bytes) for this context:
+/* Decode coefficients of `straggler_mask` (host, n bytes) for this context
+ * (IS_SGD: d = 1 for every survivor, scale 1/|J|):
  * survivors_out[0..*n_survivors_out) = the non-stragglers J in ascending order;
  * d_out[m] = the unscaled weight of coded gradient J[m]; *scale_out = the
  * common scale; decoded gradient = scale * sum_m d[m] * coded_{J[m]}.

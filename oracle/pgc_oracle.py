@@ -20,6 +20,10 @@ What it follows (Pipelined Gradient Coding, Su and Li):
     step t, sends ghat_j^(t) = sum_l g^(t-l)_{(j + (t-1-l) mod c) mod n}
     with unit coefficients, and the master forms
         ghat^(t) = (1 / (n mu)) sum_{m} ghat_{j_m}^(t),   mu = |J| c / n.
+  * Baselines of Sec. III and VI-A: gradient coding (GC) is the same placement
+    and decode with every worker evaluating all c of its partitions at the
+    current step (run(..., pipelined=False)); DGD is c = 1; IS-SGD gives each
+    worker one partition (c = 1) and averages whatever survivors arrive.
 
 The run keeps the history of iterates beta^(tau) and evaluates each coded
 gradient from the formulas above: the copy of slot l used at step t is the
@@ -61,7 +65,8 @@ import numpy as np
 FR = "FR"
 CR = "CR"
 CR_REAL = "CR_REAL"
-SCHEMES = (FR, CR, CR_REAL)
+IS_SGD = "IS_SGD"
+SCHEMES = (FR, CR, CR_REAL, IS_SGD)
 
 LOGISTIC = "logistic"
 LSQ = "lsq"
@@ -85,11 +90,14 @@ def placement(scheme, n, c):
 
     FR (Sec. III): W_i holds D_{jc}, ..., D_{jc+c-1} with j = floor(i / c); needs c | n.
     CR (Sec. III, Sec. V-B): W_i holds D_{(i+l) mod n}.
+    IS-SGD (Sec. VI-A): W_i holds D_i alone (c = 1).
     """
     if scheme not in SCHEMES:
         raise ValueError("unknown scheme %r" % (scheme,))
     if not 1 <= c <= n:
         raise ValueError("need 1 <= c <= n")
+    if scheme == IS_SGD and c != 1:
+        raise ValueError("IS-SGD gives each worker one partition (c = 1)")
     if scheme == FR:
         if n % c:
             raise ValueError("fractional repetition needs c | n")
@@ -104,19 +112,23 @@ def evaluated_slot(t, c):
     return (t - 1) % c
 
 
-def coded_terms(scheme, n, c, i, t):
+def coded_terms(scheme, n, c, i, t, pipelined=True):
     """The c copies worker W_i combines at step t, as (slot, partition, step) triples.
 
     The copy indexed l = 0..c-1 in the coded-gradient formulas of Sec. IV-A and
     Sec. V-B is partition P[i][(t-1-l) mod c] as evaluated at step t - l; a
     step below 1 means the warm-up evaluation (R4).  At t = 0 the slots
     (-1-l) mod c run over all c slots, all at step 0: the gradient-coding word.
+    Without pipelining (gradient coding) every copy is evaluated at step t.
     """
     P = placement(scheme, n, c)
     terms = []
     for l in range(c):
         slot = (t - 1 - l) % c
-        tau = t - l if t - l >= 1 else 0
+        if pipelined:
+            tau = t - l if t - l >= 1 else 0
+        else:
+            tau = t
         terms.append((slot, P[i][slot], tau))
     return terms
 
@@ -127,7 +139,7 @@ def encoding_coefficients(scheme, n, c, B=None):
     FR and PGC-CR use unit coefficients (Sec. IV-A, Sec. V-B).  The naive
     real-valued cyclic code uses c_{i,l} = B[i, (i+l) mod n] (Sec. V-A).
     """
-    if scheme in (FR, CR):
+    if scheme in (FR, CR, IS_SGD):
         return [[1.0] * c for _ in range(n)]
     if B is None:
         raise ValueError("the real-valued cyclic code needs its matrix B")
@@ -173,9 +185,14 @@ def decode_weights(scheme, n, c, J, B=None, tol=1e-9):
                 scale = 1/n (the DGD average, Sec. IV-B).
       CR:       d = 1 for every survivor; scale = 1/(n mu) = 1/(|J| c) (R7).
       CR_REAL:  minimum-norm d with B_J^T d = 1 (R8); scale = 1/n.
+      IS_SGD:   d = 1 for every survivor, however many straggle; scale = 1/|J|.
     """
     s = c - 1
     J = list(J)
+    if scheme == IS_SGD:
+        if not J:
+            raise StragglerError("every worker straggles")
+        return np.ones(len(J)), 1.0 / len(J)
     if len(J) < n - s:
         raise StragglerError("%d stragglers exceed s = %d" % (n - len(J), s))
     if scheme == FR:
@@ -323,12 +340,13 @@ class StepRecord:
 
 
 def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
-        keep_coded=True, keep_alpha=True):
+        keep_coded=True, keep_alpha=True, pipelined=True):
     """Run len(masks) PGC steps t = 0, 1, ... from beta0 and return one StepRecord per step.
 
     masks[t] is the straggler mask of step t (1 = straggles).  Step 0 is the
     warm-up: every worker evaluates all c of its partitions at beta0
     (Sec. IV-A), so its coded gradient is the gradient-coding word.
+    pipelined=False runs gradient coding: every step is such a step.
     """
     X = np.asarray(X, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
@@ -353,7 +371,7 @@ def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
         coded = []
         stale = []
         for i in range(n):
-            terms = coded_terms(scheme, n, c, i, t)
+            terms = coded_terms(scheme, n, c, i, t, pipelined)
             word = np.zeros_like(history[t])
             for slot, k, tau in terms:
                 word = word + E[i][slot] * grad(k, tau)
@@ -367,7 +385,7 @@ def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
         ghat = scale * acc
         beta_next = history[t] - lr * ghat
         history[t + 1] = beta_next
-        evaluated = ([P[i][l] for i in range(n) for l in range(c)] if t == 0
+        evaluated = ([P[i][l] for i in range(n) for l in range(c)] if (t == 0 or not pipelined)
                      else [P[i][evaluated_slot(t, c)] for i in range(n)])
         records.append(StepRecord(
             t=t, survivors=J, d=np.asarray(d), scale=scale, ghat=ghat, beta=beta_next,

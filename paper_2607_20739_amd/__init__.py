@@ -13,12 +13,13 @@ from . import _lib
 class PGCSession:
     """A configured PGC context bound to a torch-allocated workspace on one GPU.
 
-    scheme: "FR", "CR" or "CR_REAL"; model: "logistic", "lsq" or "mlp".
+    scheme: "FR", "CR", "CR_REAL" or "IS_SGD"; model: "logistic", "lsq" or "mlp".
+    pipelined=False runs gradient coding instead (every slot evaluated each step).
     q (the parameter length) follows from the model shape.
     """
 
     def __init__(self, scheme, n, c, model, N, d_in, hidden=0, classes=0, code_seed=0,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, pipelined=True):
         import torch
         self.n, self.c, self.N, self.d_in = int(n), int(c), int(N), int(d_in)
         self.scheme, self.model = scheme, model
@@ -43,6 +44,8 @@ class PGCSession:
             self.ctx = None
             raise
         self.n_coded = _lib.pgc_num_coded(self.ctx)
+        if not pipelined:
+            _lib.pgc_set_pipelining(self.ctx, False)
 
     def step(self, X, y, w, straggler_mask, lr):
         """One step; X, y, w are GPU tensors holding at least N*d_in, N and q elements."""

@@ -13,7 +13,7 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpgc.so")
 
-PGC_FR, PGC_CR, PGC_CR_REAL = 0, 1, 2
+PGC_FR, PGC_CR, PGC_CR_REAL, PGC_IS_SGD = 0, 1, 2, 3
 PGC_LOGISTIC, PGC_LSQ, PGC_MLP = 0, 1, 2
 PGC_OK, PGC_EINVAL, PGC_ESTRAGGLERS, PGC_ESINGULAR, PGC_EDEVICE, PGC_ESTATE = 0, -1, -2, -3, -4, -5
 PGC_POLICY_EXACT, PGC_POLICY_UNIFORM_COUNT, PGC_POLICY_BERNOULLI = 0, 1, 2
@@ -21,7 +21,7 @@ PGC_KERNEL_GRADIENT, PGC_KERNEL_REDUCE, PGC_KERNEL_CODE = 0, 1, 2
 PGC_KERNEL_MLP_CAST, PGC_KERNEL_MLP_FORWARD, PGC_KERNEL_MLP_HEAD, PGC_KERNEL_MLP_WGRAD = 3, 4, 5, 6
 PGC_MAX_N = 256
 
-SCHEMES = {"FR": PGC_FR, "CR": PGC_CR, "CR_REAL": PGC_CR_REAL}
+SCHEMES = {"FR": PGC_FR, "CR": PGC_CR, "CR_REAL": PGC_CR_REAL, "IS_SGD": PGC_IS_SGD}
 MODELS = {"logistic": PGC_LOGISTIC, "lsq": PGC_LSQ, "mlp": PGC_MLP}
 
 
@@ -46,6 +46,7 @@ _U8P = ctypes.POINTER(ctypes.c_uint8)
 _SIGNATURES = {
     "pgc_init": (ctypes.c_int, [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int64]),
     "pgc_configure": (ctypes.c_int, [_P, ctypes.POINTER(pgc_config)]),
+    "pgc_set_pipelining": (ctypes.c_int, [_P, ctypes.c_int]),
     "pgc_set_stream": (ctypes.c_int, [_P, _P]),
     "pgc_workspace_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "pgc_bind_workspace": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
@@ -130,6 +131,11 @@ def pgc_init(scheme, n, c, d):
 def pgc_configure(ctx, model, N, d_in, hidden=0, classes=0, code_seed=0):
     cfg = pgc_config(MODELS.get(model, model), int(d_in), int(N), int(hidden), int(classes), int(code_seed))
     _check(lib().pgc_configure(ctx, ctypes.byref(cfg)), ctx)
+
+
+def pgc_set_pipelining(ctx, enabled):
+    """True: pipelined gradient coding (default); False: gradient coding."""
+    _check(lib().pgc_set_pipelining(ctx, 1 if enabled else 0), ctx)
 
 
 def pgc_set_stream(ctx, stream):

@@ -255,6 +255,16 @@ DecodeStatus decode_coefficients(int scheme, int n, int c, const std::vector<dou
   for (int i = 0; i < n; ++i)
     if (mask[i] == 0) out->survivors.push_back(i);
   const int nj = static_cast<int>(out->survivors.size());
+  if (scheme == kISSGD) {
+    // Ignore-straggler SGD: the master averages whatever arrived (Sec. VI-A).
+    if (nj < 1) {
+      if (err) *err = "every worker straggles";
+      return kDecodeStragglers;
+    }
+    out->d.assign(nj, 1.0);
+    out->scale = 1.0 / nj;
+    return kDecodeOk;
+  }
   const int s = c - 1;
   if (nj < n - s) {
     if (err) *err = std::to_string(n - nj) + " stragglers exceed s = " + std::to_string(s);

@@ -9,10 +9,10 @@
 
 namespace pgc {
 
-enum Scheme { kFR = 0, kCR = 1, kCRReal = 2 };
+enum Scheme { kFR = 0, kCR = 1, kCRReal = 2, kISSGD = 3 };
 
 // Partition held by worker i in slot l (Sec. III).
-//   FR: (i / c) * c + l          CR: (i + l) mod n
+//   FR: (i / c) * c + l          CR (and IS-SGD, c = 1): (i + l) mod n
 int held_partition(int scheme, int n, int c, int i, int l);
 
 // Slot every worker evaluates at pipelined step t >= 1 (Sec. IV-A, Sec. V-B).
@@ -53,10 +53,12 @@ struct Decode {
 
 enum DecodeStatus { kDecodeOk = 0, kDecodeStragglers = 1, kDecodeSingular = 2 };
 
-// Decode coefficients for a straggler mask (Sec. IV-A, Sec. V-A, Sec. V-B):
+// Decode coefficients for a straggler mask (Sec. IV-A, Sec. V-A, Sec. V-B,
+// Sec. VI-A):
 //   FR:      1 for the lowest-index survivor of each group; scale 1/n.
 //   CR:      1 for every survivor; scale 1/(|J| c).
 //   CR_REAL: minimum-norm d with B_J^T d = 1, residual <= 1e-9; scale 1/n.
+//   IS_SGD:  1 for every survivor (any number of stragglers below n); scale 1/|J|.
 DecodeStatus decode_coefficients(int scheme, int n, int c, const std::vector<double>& B,
                                  const uint8_t* mask, Decode* out, std::string* err);
 

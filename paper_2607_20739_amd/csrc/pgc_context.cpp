@@ -82,6 +82,7 @@ struct pgc_ctx {
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
   int64_t t = 0;
+  bool pipelined = true;      // false: gradient coding (every slot evaluated each step)
   std::string err;
   unsigned timing = 0;        // bit k: time kernel k
   std::vector<Timed> pending;
@@ -243,9 +244,11 @@ const char* pgc_last_error(const pgc_ctx* ctx) {
 int pgc_init(pgc_ctx** out, int scheme, int n, int c, int64_t d) {
   if (out == nullptr) return PGC_EINVAL;
   *out = nullptr;
-  if (scheme != PGC_FR && scheme != PGC_CR && scheme != PGC_CR_REAL) return PGC_EINVAL;
+  if (scheme != PGC_FR && scheme != PGC_CR && scheme != PGC_CR_REAL && scheme != PGC_IS_SGD)
+    return PGC_EINVAL;
   if (n < 1 || n > PGC_MAX_N || c < 1 || c > n || d < 1) return PGC_EINVAL;
   if (scheme == PGC_FR && n % c != 0) return PGC_EINVAL;
+  if (scheme == PGC_IS_SGD && c != 1) return PGC_EINVAL;
   pgc_ctx* ctx = new (std::nothrow) pgc_ctx;
   if (ctx == nullptr) return PGC_EINVAL;
   ctx->scheme = scheme;
@@ -308,6 +311,12 @@ int pgc_configure(pgc_ctx* ctx, const pgc_config* cfg) {
   }
   compute_layout(ctx);
   ctx->configured = true;
+  return PGC_OK;
+}
+
+int pgc_set_pipelining(pgc_ctx* ctx, int enabled) {
+  if (ctx == nullptr) return PGC_EINVAL;
+  ctx->pipelined = enabled != 0;
   return PGC_OK;
 }
 
@@ -452,8 +461,7 @@ pgc::CodeArgs code_args(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr
 // The linear models' step: the gradient kernel (a4), then one launch that
 // folds its partials into the ring (a5) and runs encode, decode and update (a6-a8).
 int linear_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::Decode& dec, float lr,
-                int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
-  const bool warm = ctx->t == 0;
+                bool warm, int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
   const Grid& grid = warm ? ctx->warm : ctx->pipe;
   pgc::LinearGradArgs ga{};
   ga.X = static_cast<const float*>(X);
@@ -493,8 +501,7 @@ int linear_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc:
 // a4-a5 for the MLP: cast, forward, head, weight gradient, small-part reduce,
 // then copies of the slot into the other planes at the CR warm-up.
 int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::Decode& dec, float lr,
-             int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
-  const bool warm = ctx->t == 0;
+             bool warm, int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
   const Grid& hg = warm ? ctx->head_warm : ctx->head_pipe;
   const int32_t d_in = ctx->cfg.d_in, hidden = ctx->cfg.hidden, classes = ctx->cfg.classes;
   const int64_t w1 = static_cast<int64_t>(d_in) * hidden;
@@ -615,7 +622,8 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
   }
   const int c = ctx->c;
   const bool fr = ctx->scheme == PGC_FR;
-  const bool warm = ctx->t == 0;
+  // The warm-up step, and every step of gradient coding, evaluates all slots.
+  const bool warm = ctx->t == 0 || !ctx->pipelined;
   const int o = warm ? 0 : pgc::evaluated_slot(ctx->t, c);
   // Evaluated partitions: all at the warm-up; one per FR group (jc + o) or
   // every partition for CR at t >= 1.
@@ -631,14 +639,14 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
     if (reinterpret_cast<uintptr_t>(X) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
         reinterpret_cast<uintptr_t>(w) % 4 != 0)
       return fail(ctx, PGC_EINVAL, "MLP: X must be 16-byte aligned, y and w 4-byte aligned");
-    st = mlp_step(ctx, X, y, w, dec, lr, part_stride, part_offset, plane_first, plane_count);
+    st = mlp_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
   } else {
     const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
                            reinterpret_cast<uintptr_t>(w) % 16 == 0;
     if (!pgc::linear_grad_shape(static_cast<int>(ctx->d), aligned16).supported)
       return fail(ctx, PGC_EINVAL, "d = " + std::to_string(ctx->d) +
                                        " needs d % 4 == 0 and 16-byte aligned X and w");
-    st = linear_step(ctx, X, y, w, dec, lr, part_stride, part_offset, plane_first, plane_count);
+    st = linear_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
   }
   if (st != PGC_OK) return st;
   ctx->t += 1;

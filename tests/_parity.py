@@ -6,7 +6,7 @@ import numpy as np
 from oracle import pgc_oracle as O
 from oracle import rng as R
 
-SCHEMES = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
+SCHEMES = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL, "IS_SGD": O.IS_SGD}
 
 # Floating-point bar of the fp32 path (normwise, per step, per vector):
 #   max_i |gpu_i - oracle_i| / max_i |oracle_i| <= 1e-5.
@@ -31,17 +31,17 @@ def oracle_code_matrix(w):
     return O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
 
 
-def oracle_run(w, X, y, beta0, masks, lr=None, keep_coded=False):
+def oracle_run(w, X, y, beta0, masks, lr=None, keep_coded=False, pipelined=True):
     shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
     return O.run(SCHEMES[w.scheme], w.model, w.n, w.c, X, y, beta0, w.lr if lr is None else lr,
                  masks, B=oracle_code_matrix(w), shape=shape, keep_coded=keep_coded,
-                 keep_alpha=False)
+                 keep_alpha=False, pipelined=pipelined)
 
 
-def gpu_session(w, device="cuda"):
+def gpu_session(w, device="cuda", pipelined=True):
     import paper_2607_20739_amd as P
     return P.PGCSession(w.scheme, w.n, w.c, w.model, w.N, w.d, hidden=w.hidden, classes=w.classes,
-                        code_seed=w.code_seed, device=device)
+                        code_seed=w.code_seed, device=device, pipelined=pipelined)
 
 
 def gpu_masks(w, steps=None):
@@ -50,10 +50,10 @@ def gpu_masks(w, steps=None):
     return [P.pgc_make_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(steps)]
 
 
-def gpu_run(w, X, y, beta0, masks, lr=None, keep=("ghat", "w"), read_coded=False):
+def gpu_run(w, X, y, beta0, masks, lr=None, keep=("ghat", "w"), read_coded=False, pipelined=True):
     """Run the HIP path; returns one dict per step with host copies of the kept vectors."""
     import torch
-    sess = gpu_session(w, X.device)
+    sess = gpu_session(w, X.device, pipelined=pipelined)
     wv = beta0.clone()
     out = []
     try:

@@ -17,7 +17,7 @@ from oracle import pgc_oracle as O
 from oracle import rng as R
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SCHEME_NAMES = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
+SCHEME_NAMES = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL, "IS_SGD": O.IS_SGD}
 
 
 def _declared_symbols():
@@ -43,7 +43,7 @@ def _ctx(scheme, n, c, d=8, model="lsq", N=None, code_seed=0):
 
 CASES = [("FR", 4, 2), ("FR", 32, 4), ("FR", 6, 6), ("FR", 5, 1), ("CR", 8, 3), ("CR", 64, 4),
          ("CR", 128, 8), ("CR", 7, 7), ("CR_REAL", 8, 3), ("CR_REAL", 12, 6), ("CR_REAL", 4, 2),
-         ("CR_REAL", 5, 1)]
+         ("CR_REAL", 5, 1), ("IS_SGD", 12, 1), ("IS_SGD", 1, 1)]
 
 
 @pytest.mark.parametrize("scheme,n,c", CASES)
@@ -114,6 +114,27 @@ def test_decode_coefficients_match_the_oracle_for_every_admissible_mask(scheme, 
                     assert d.tolist() == d_or.tolist()
     finally:
         P.pgc_destroy(ctx)
+
+
+def test_is_sgd_decode_ignores_any_number_of_stragglers():
+    n = 6
+    ctx = _ctx("IS_SGD", n, 1)
+    try:
+        for k in range(n):
+            for strag in itertools.combinations(range(n), k):
+                mask = np.zeros(n, np.uint8)
+                mask[list(strag)] = 1
+                surv, d, scale = P.pgc_decode_coeffs(ctx, mask, n)
+                d_or, scale_or = O.decode_weights(O.IS_SGD, n, 1, O.survivors(mask))
+                assert surv.tolist() == O.survivors(mask)
+                assert d.tolist() == d_or.tolist() and scale == scale_or
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_decode_coeffs(ctx, np.ones(n, np.uint8), n)
+        assert e.value.status == P.PGC_ESTRAGGLERS
+    finally:
+        P.pgc_destroy(ctx)
+    with pytest.raises(P.PGCError):
+        P.pgc_init("IS_SGD", 6, 2, 8)        # IS-SGD holds one partition per worker
 
 
 def test_error_codes():

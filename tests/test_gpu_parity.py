@@ -40,15 +40,15 @@ def _to_host(*tensors):
     return [t.cpu().numpy() for t in tensors]
 
 
-def _check_trajectory(w, X, y, beta0, steps=None, X_host=None):
+def _check_trajectory(w, X, y, beta0, steps=None, X_host=None, pipelined=True):
     masks_gpu = gpu_masks(w, steps)
     masks_or = oracle_masks(w, steps)
     for t, (a, b) in enumerate(zip(masks_gpu, masks_or)):
         assert a.tolist() == b.tolist(), "mask of step %d differs" % t
-    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu)
+    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu, pipelined=pipelined)
     Xh = X_host if X_host is not None else X.cpu().numpy()
     yh, bh = _to_host(y, beta0)
-    recs_or = oracle_run(w, Xh, yh, bh, masks_or)
+    recs_or = oracle_run(w, Xh, yh, bh, masks_or, pipelined=pipelined)
     worst = 0.0
     for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
         e_g = normwise_error(g["ghat"], o.ghat)
@@ -118,6 +118,39 @@ def test_edge_case_trajectory_matches_oracle(w):
     _announce("%s N=%d d=%d" % (w.name, w.N, w.d))
     X, y, beta0 = make_inputs(w, device="cuda")
     _check_trajectory(w, X, y, beta0)
+
+
+BASELINES = [
+    # gradient coding (every slot evaluated each step) for the three codes
+    (Workload("gc_fr_logistic", "FR", "logistic", n=8, c=4, N=8 * 500, d=1024, lr=0.05, steps=8,
+              policy=POLICY_UNIFORM_COUNT, cap=3, seed=41), False),
+    (Workload("gc_real_lsq", "CR_REAL", "lsq", n=8, c=3, N=8 * 700, d=256, lr=0.02, steps=8,
+              policy=POLICY_UNIFORM_COUNT, cap=2, seed=42, code_seed=5), False),
+    (Workload("gc_cr_logistic", "CR", "logistic", n=6, c=3, N=6 * 300, d=4096, lr=0.02, steps=6,
+              policy=POLICY_UNIFORM_COUNT, cap=2, seed=43), False),
+    # ignore-straggler SGD with up to n - 1 stragglers
+    (Workload("is_sgd_logistic", "IS_SGD", "logistic", n=12, c=1, N=12 * 200, d=512, lr=0.1, steps=10,
+              policy=POLICY_UNIFORM_COUNT, cap=11, seed=44), True),
+    (Workload("is_sgd_mlp", "IS_SGD", "mlp", n=4, c=1, N=4 * 64, d=64, lr=0.05, steps=5,
+              policy=POLICY_EXACT, cap=2, seed=45, hidden=256, classes=10), True),
+]
+
+
+@pytest.mark.parametrize("w,pipelined", BASELINES, ids=[b[0].name for b in BASELINES])
+def test_baseline_trajectory_matches_oracle(w, pipelined):
+    _announce("%s pipelined=%s" % (w.name, pipelined))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    if w.model == "mlp":
+        masks_gpu, masks_or = gpu_masks(w), oracle_masks(w)
+        assert [m.tolist() for m in masks_gpu] == [m.tolist() for m in masks_or]
+        recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu, pipelined=pipelined)
+        recs_or = oracle_run(w, X.float().cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy(), masks_or,
+                             pipelined=pipelined)
+        for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
+            assert normwise_error(g["ghat"], o.ghat) <= 2e-2, t
+            assert normwise_error(g["w"], o.beta) <= 2e-2, t
+        return
+    _check_trajectory(w, X, y, beta0, pipelined=pipelined)
 
 
 def test_unaligned_features_take_the_scalar_path():

@@ -441,3 +441,64 @@ def test_null_space_generator_entries():
     assert H.shape == (3, 9)
     assert np.all(H[:, :-1] >= -1.0) and np.all(H[:, :-1] < 1.0)
     assert np.array_equal(H[:, -1], -np.array([sum(H[a, :-1].tolist()) for a in range(3)]))
+
+
+# --------------------------------------------------------------------------
+# Baselines: gradient coding (no pipelining), DGD and IS-SGD (Sec. III, VI)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("scheme,n,c", [(O.FR, 6, 3), (O.FR, 8, 2), (O.CR_REAL, 6, 3), (O.CR_REAL, 5, 2)])
+def test_gradient_coding_coincides_with_dgd(scheme, n, c):
+    """Sec. VI-B: GC recovers the same aggregated gradient as DGD, whatever straggles."""
+    N, d, T, lr = n * 10, 5, 8, 0.3
+    X, y, beta0 = _data(O.LOGISTIC, N, d, seed=40 + n)
+    B = _code_matrix(n, c, seed=n) if scheme == O.CR_REAL else None
+    masks = [R.straggler_mask(7, t, R.POLICY_UNIFORM_COUNT, n, c - 1) for t in range(T)]
+    recs = O.run(scheme, O.LOGISTIC, n, c, X, y, beta0, lr, masks, B=B, pipelined=False)
+    beta = beta0.copy()
+    for t in range(T):
+        beta = beta - lr * _full_gradient_linear(O.LOGISTIC, X, y, beta)
+        np.testing.assert_allclose(recs[t].beta, beta, rtol=1e-9, atol=1e-12)
+
+
+def test_gradient_coding_cr_unit_without_stragglers_is_dgd():
+    n, c = 6, 3
+    X, y, beta0 = _data(O.LSQ, n * 8, 4, seed=51)
+    recs = O.run(O.CR, O.LSQ, n, c, X, y, beta0, 0.2, [np.zeros(n, np.uint8)] * 5, pipelined=False)
+    beta = beta0.copy()
+    for r in recs:
+        beta = beta - 0.2 * _full_gradient_linear(O.LSQ, X, y, beta)
+        np.testing.assert_allclose(r.beta, beta, rtol=1e-12, atol=1e-14)
+
+
+def test_is_sgd_without_stragglers_is_dgd():
+    """Sec. VI-A: IS-SGD is DGD when s = 0."""
+    n = 5
+    X, y, beta0 = _data(O.LOGISTIC, n * 12, 6, seed=52)
+    recs = O.run(O.IS_SGD, O.LOGISTIC, n, 1, X, y, beta0, 0.4, [np.zeros(n, np.uint8)] * 6)
+    beta = beta0.copy()
+    for r in recs:
+        beta = beta - 0.4 * _full_gradient_linear(O.LOGISTIC, X, y, beta)
+        np.testing.assert_allclose(r.beta, beta, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("n,s", [(5, 1), (6, 3), (7, 6)])
+def test_is_sgd_is_unbiased_over_straggler_sets(n, s):
+    """Averaging the survivors' gradients is unbiased over uniformly chosen straggler sets."""
+    X, y, beta0 = _data(O.LSQ, n * 6, 4, seed=53)
+    g_full = _full_gradient_linear(O.LSQ, X, y, beta0)
+    acc = np.zeros(4)
+    count = 0
+    for strag in itertools.combinations(range(n), s):
+        mask = np.zeros(n, np.uint8)
+        mask[list(strag)] = 1
+        acc += O.run(O.IS_SGD, O.LSQ, n, 1, X, y, beta0, 0.0, [mask])[0].ghat
+        count += 1
+    np.testing.assert_allclose(acc / count, g_full, rtol=1e-12, atol=1e-15)
+
+
+def test_is_sgd_rejects_an_empty_survivor_set_and_c_above_one():
+    with pytest.raises(O.StragglerError):
+        O.decode_weights(O.IS_SGD, 4, 1, [])
+    with pytest.raises(ValueError):
+        O.placement(O.IS_SGD, 4, 2)
