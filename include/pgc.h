@@ -63,7 +63,10 @@ enum pgc_status {
 enum pgc_mask_policy {
   PGC_POLICY_EXACT = 0,         /* exactly `cap` stragglers, uniformly chosen */
   PGC_POLICY_UNIFORM_COUNT = 1, /* count uniform in {0..cap}, then uniformly chosen */
-  PGC_POLICY_BERNOULLI = 2      /* each worker with probability p, at most `cap` kept */
+  PGC_POLICY_BERNOULLI = 2,     /* each worker with probability p, at most `cap` kept */
+  PGC_POLICY_SLOWEST = 3        /* the `cap` slowest under i.i.d. exponential delays: worker i
+                                   draws u_i (its delay is -mean ln(1 - u_i)); the `cap`
+                                   largest u_i straggle, lower index first on ties */
 };
 
 /* Kernels whose GPU time pgc_kernel_time reports. */
@@ -185,6 +188,21 @@ int pgc_num_coded(const pgc_ctx* ctx, int32_t* out);
  * PGC_POLICY_BERNOULLI, probability p.  Independent of any context. */
 int pgc_make_mask(uint64_t seed, int64_t t, int policy, int n, int cap, double p,
                   uint8_t* out);
+
+/* One step of the simulated straggler model of Sec. VI-B (independent of any
+ * context; host only).  Worker i draws u_i (draw i of step t of the SplitMix64
+ * stream `seed`, as for pgc_make_mask) and finishes after
+ * compute_seconds + delay_i with the exponential delay
+ * delay_i = -mean_delay * ln(1 - u_i).  The master waits for the n - s fastest
+ * workers: `mask` (n bytes) marks the s others (identical to pgc_make_mask with
+ * PGC_POLICY_SLOWEST and cap s), `*step_seconds` is the (n - s)-th smallest
+ * finish time (s = 0: the slowest worker, as DGD waits for).  `delays` (n
+ * doubles, may be NULL) receives every delay_i.  compute_seconds is the
+ * worker's compute time for the step, equal across workers.  PGC_EINVAL when
+ * n is outside [1, PGC_MAX_N], s outside [0, n - 1], t < 0, mean_delay or
+ * compute_seconds negative or not finite, or mask / step_seconds is NULL. */
+int pgc_delay_step(uint64_t seed, int64_t t, int n, int s, double mean_delay,
+                   double compute_seconds, uint8_t* mask, double* delays, double* step_seconds);
 
 /* Output `index` (0-based) of the SplitMix64 stream seeded with `seed`. */
 int pgc_splitmix64(uint64_t seed, uint64_t index, uint64_t* out);

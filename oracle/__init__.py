@@ -7,7 +7,8 @@ the two share no code: no kernels, headers, helpers or table generators.
 
 Modules:
   rng         -- SplitMix64 and the straggler-mask / encoding-matrix draws,
-                 written from the generator's published definition.
+                 written from the generator's published definition, and the
+                 simulated cluster step with exponential worker delays.
   pgc_oracle  -- placement, schedule, coded gradients, decoding and the
                  update, step by step in the paper's order and notation.
 

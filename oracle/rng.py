@@ -29,7 +29,15 @@ worker, Sec. VI-B; here the straggler set itself is drawn):
                     of the straggler list (draws n, n+1, ...) keeps the first
                     cap of them.  Each worker is equally likely to straggle,
                     which the unbiasedness argument of Sec. V-B assumes.
+  SLOWEST(cap)      worker i draws u_i = uniform01(draw_i); the cap workers with
+                    the largest u_i straggle (ties: the lower index straggles).
+                    With i.i.d. exponential delays -mean * ln(1 - u_i) on top of
+                    equal compute times these are exactly the workers the
+                    master does not wait for when it takes the n - cap fastest
+                    (the delay model of Sec. VI-B).
 """
+
+import math
 
 import numpy as np
 
@@ -39,6 +47,7 @@ GAMMA = 0x9E3779B97F4A7C15
 POLICY_EXACT = 0
 POLICY_UNIFORM_COUNT = 1
 POLICY_BERNOULLI = 2
+POLICY_SLOWEST = 3
 
 
 def mix64(z):
@@ -86,11 +95,38 @@ def straggler_mask(seed, t, policy, n, cap, p=0.0):
         chosen = [i for i in range(n) if uniform01(step_draw(seed, t, i)) < p]
         if len(chosen) > cap:
             chosen = _partial_shuffle(seed, t, n, chosen, cap)
+    elif policy == POLICY_SLOWEST:
+        u = [uniform01(step_draw(seed, t, i)) for i in range(n)]
+        order = sorted(range(n), key=lambda i: (-u[i], i))
+        chosen = order[:min(cap, n)]
     else:
         raise ValueError("unknown straggler policy %r" % (policy,))
     mask = np.zeros(n, dtype=np.uint8)
     mask[list(chosen)] = 1
     return mask
+
+
+def delay_draws(seed, t, n):
+    """The uniforms u_i behind the SLOWEST policy's delays at step t."""
+    return [uniform01(step_draw(seed, t, i)) for i in range(n)]
+
+
+def delay_step(seed, t, n, s, mean_delay, compute_seconds=0.0):
+    """One step of the simulated cluster of Sec. VI-B.
+
+    Every worker adds an independent exponential delay of mean `mean_delay`
+    to its compute time; the master continues once n - s workers have
+    finished (s = 0: it waits for all of them, as DGD must).  The delay of
+    worker i is the inverse exponential CDF at its draw u_i.
+    Returns (mask uint8[n] of the s workers not waited for, delays, seconds).
+    """
+    u = delay_draws(seed, t, n)
+    delays = [-mean_delay * math.log1p(-ui) for ui in u]
+    finish = [compute_seconds + dl for dl in delays]
+    waited = sorted(range(n), key=lambda i: (u[i], -i))[:n - s]
+    mask = np.ones(n, dtype=np.uint8)
+    mask[waited] = 0
+    return mask, np.array(delays), max(finish[i] for i in waited)
 
 
 def null_space_generator(seed, s, n):

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpgc.so")
 PGC_FR, PGC_CR, PGC_CR_REAL, PGC_IS_SGD = 0, 1, 2, 3
 PGC_LOGISTIC, PGC_LSQ, PGC_MLP = 0, 1, 2
 PGC_OK, PGC_EINVAL, PGC_ESTRAGGLERS, PGC_ESINGULAR, PGC_EDEVICE, PGC_ESTATE = 0, -1, -2, -3, -4, -5
-PGC_POLICY_EXACT, PGC_POLICY_UNIFORM_COUNT, PGC_POLICY_BERNOULLI = 0, 1, 2
+PGC_POLICY_EXACT, PGC_POLICY_UNIFORM_COUNT, PGC_POLICY_BERNOULLI, PGC_POLICY_SLOWEST = 0, 1, 2, 3
 PGC_KERNEL_GRADIENT, PGC_KERNEL_REDUCE, PGC_KERNEL_CODE = 0, 1, 2
 PGC_KERNEL_MLP_CAST, PGC_KERNEL_MLP_FORWARD, PGC_KERNEL_MLP_HEAD, PGC_KERNEL_MLP_WGRAD = 3, 4, 5, 6
 PGC_MAX_N = 256
@@ -58,6 +58,8 @@ _SIGNATURES = {
     "pgc_num_coded": (ctypes.c_int, [_P, _I32P]),
     "pgc_make_mask": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                      ctypes.c_int, ctypes.c_double, _U8P]),
+    "pgc_delay_step": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_double, ctypes.c_double, _U8P, _F64P, _F64P]),
     "pgc_splitmix64": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(ctypes.c_uint64)]),
     "pgc_read_ring": (ctypes.c_int, [_P, ctypes.c_int, ctypes.c_int, _P]),
     "pgc_read_coded": (ctypes.c_int, [_P, ctypes.c_int, _P]),
@@ -203,6 +205,17 @@ def pgc_make_mask(seed, t, policy, n, cap, p=0.0):
     _check(lib().pgc_make_mask(int(seed), int(t), int(policy), int(n), int(cap), float(p),
                                out.ctypes.data_as(_U8P)))
     return out
+
+
+def pgc_delay_step(seed, t, n, s, mean_delay, compute_seconds=0.0):
+    """Simulated straggler step: (mask uint8[n], delays float64[n], step_seconds)."""
+    mask = np.zeros(n, dtype=np.uint8)
+    delays = np.zeros(n, dtype=np.float64)
+    step = ctypes.c_double()
+    _check(lib().pgc_delay_step(int(seed), int(t), int(n), int(s), float(mean_delay),
+                                float(compute_seconds), mask.ctypes.data_as(_U8P),
+                                delays.ctypes.data_as(_F64P), ctypes.byref(step)))
+    return mask, delays, step.value
 
 
 def pgc_splitmix64(seed, index):

@@ -62,11 +62,37 @@ bool make_mask(uint64_t seed, int64_t t, int policy, int n, int cap, double p,
       if (uniform01(step_draw(seed, t, static_cast<uint64_t>(i))) < p) chosen.push_back(i);
     if (static_cast<int>(chosen.size()) > cap)
       partial_shuffle(seed, t, static_cast<uint64_t>(n), &chosen, cap);
+  } else if (policy == 3) {
+    // The cap workers with the largest delay draws (lower index first on ties).
+    std::vector<double> u(n);
+    for (int i = 0; i < n; ++i) u[i] = uniform01(step_draw(seed, t, static_cast<uint64_t>(i)));
+    chosen.resize(n);
+    std::iota(chosen.begin(), chosen.end(), 0);
+    std::stable_sort(chosen.begin(), chosen.end(), [&](int a, int b) { return u[a] > u[b]; });
+    chosen.resize(std::min(cap, n));
   } else {
     return false;
   }
   std::fill(out, out + n, uint8_t{0});
   for (int i : chosen) out[i] = 1;
+  return true;
+}
+
+bool delay_step(uint64_t seed, int64_t t, int n, int s, double mean_delay, double compute_seconds,
+                uint8_t* mask, double* delays, double* step_seconds) {
+  if (n <= 0 || s < 0 || s >= n || t < 0 || mask == nullptr || step_seconds == nullptr) return false;
+  if (!(mean_delay >= 0.0 && std::isfinite(mean_delay))) return false;
+  if (!(compute_seconds >= 0.0 && std::isfinite(compute_seconds))) return false;
+  // Inverse-CDF exponential delays; the same uniforms rank the workers for the
+  // mask, so the stragglers are exactly the s largest delays.
+  std::vector<double> delay(n);
+  for (int i = 0; i < n; ++i)
+    delay[i] = -mean_delay * std::log1p(-uniform01(step_draw(seed, t, static_cast<uint64_t>(i))));
+  if (!make_mask(seed, t, 3, n, s, 0.0, mask)) return false;
+  std::vector<double> sorted(delay);
+  std::sort(sorted.begin(), sorted.end());
+  *step_seconds = compute_seconds + sorted[n - s - 1];
+  if (delays != nullptr) std::copy(delay.begin(), delay.end(), delays);
   return true;
 }
 

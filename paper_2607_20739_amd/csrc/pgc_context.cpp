@@ -416,6 +416,13 @@ int pgc_make_mask(uint64_t seed, int64_t t, int policy, int n, int cap, double p
   return pgc::make_mask(seed, t, policy, n, cap, p, out) ? PGC_OK : PGC_EINVAL;
 }
 
+int pgc_delay_step(uint64_t seed, int64_t t, int n, int s, double mean_delay, double compute_seconds,
+                   uint8_t* mask, double* delays, double* step_seconds) {
+  if (n < 1 || n > PGC_MAX_N) return PGC_EINVAL;
+  return pgc::delay_step(seed, t, n, s, mean_delay, compute_seconds, mask, delays, step_seconds)
+             ? PGC_OK : PGC_EINVAL;
+}
+
 int pgc_splitmix64(uint64_t seed, uint64_t index, uint64_t* out) {
   if (out == nullptr) return PGC_EINVAL;
   *out = pgc::splitmix64(seed, index);

@@ -71,13 +71,36 @@ def test_splitmix64_matches_the_oracle():
 @pytest.mark.parametrize("policy,n,cap,p", [
     (R.POLICY_EXACT, 4, 1, 0.0), (R.POLICY_UNIFORM_COUNT, 8, 2, 0.0), (R.POLICY_BERNOULLI, 32, 3, 0.05),
     (R.POLICY_BERNOULLI, 64, 3, 0.05), (R.POLICY_BERNOULLI, 128, 7, 0.04), (R.POLICY_BERNOULLI, 16, 2, 0.5),
-    (R.POLICY_EXACT, 256, 255, 0.0), (R.POLICY_UNIFORM_COUNT, 1, 0, 0.0)])
+    (R.POLICY_EXACT, 256, 255, 0.0), (R.POLICY_UNIFORM_COUNT, 1, 0, 0.0), (R.POLICY_SLOWEST, 12, 3, 0.0),
+    (R.POLICY_SLOWEST, 256, 17, 0.0), (R.POLICY_SLOWEST, 5, 0, 0.0)])
 def test_masks_match_the_oracle_bit_for_bit(policy, n, cap, p):
     for seed in [(1 << 32) | 1, (5 << 32) | 1, 99]:
         for t in range(60):
             a = P.pgc_make_mask(seed, t, policy, n, cap, p)
             b = R.straggler_mask(seed, t, policy, n, cap, p)
             assert a.tolist() == b.tolist(), (seed, t)
+
+
+@pytest.mark.parametrize("n,s,mean,compute", [(12, 1, 1.0, 1.0), (12, 3, 2.0, 4.0), (12, 0, 1.0, 1.0),
+                                               (256, 7, 0.5, 0.0), (1, 0, 1.0, 0.0), (8, 7, 0.0, 2.0)])
+def test_delay_steps_match_the_oracle(n, s, mean, compute):
+    for seed in [(2 << 32) | 1, 31]:
+        for t in range(40):
+            mask, delays, sec = P.pgc_delay_step(seed, t, n, s, mean, compute)
+            m_or, d_or, sec_or = R.delay_step(seed, t, n, s, mean, compute)
+            assert mask.tolist() == m_or.tolist()
+            np.testing.assert_allclose(delays, d_or, rtol=1e-15, atol=0.0)
+            assert sec == pytest.approx(sec_or, rel=1e-15, abs=0.0)
+            assert mask.tolist() == P.pgc_make_mask(seed, t, P.PGC_POLICY_SLOWEST, n, s).tolist()
+
+
+def test_delay_step_rejects_bad_arguments():
+    for args in [(1, 0, 4, 4, 1.0, 0.0), (1, 0, 4, -1, 1.0, 0.0), (1, -1, 4, 1, 1.0, 0.0),
+                 (1, 0, 4, 1, -1.0, 0.0), (1, 0, 4, 1, float("nan"), 0.0), (1, 0, 4, 1, 1.0, -2.0),
+                 (1, 0, 0, 0, 1.0, 0.0), (1, 0, 257, 1, 1.0, 0.0)]:
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_delay_step(*args)
+        assert e.value.status == P.PGC_EINVAL
 
 
 @pytest.mark.parametrize("n,c,seed", [(4, 2, 1), (8, 3, 2), (12, 6, 3), (5, 1, 4), (16, 5, 9)])

@@ -421,7 +421,7 @@ def test_masks_make_every_worker_equally_likely_to_straggle():
     from scipy.stats import chisquare, binomtest
     n, T = 8, 20000
     for policy, cap, p in [(R.POLICY_EXACT, 1, 0.0), (R.POLICY_UNIFORM_COUNT, 2, 0.0),
-                           (R.POLICY_BERNOULLI, 3, 0.1)]:
+                           (R.POLICY_BERNOULLI, 3, 0.1), (R.POLICY_SLOWEST, 2, 0.0)]:
         freq = np.zeros(n)
         counts = np.zeros(cap + 1)
         for t in range(T):
@@ -434,6 +434,48 @@ def test_masks_make_every_worker_equally_likely_to_straggle():
         if policy == R.POLICY_BERNOULLI:
             # P(count = 0) = (1 - p)^n for the Bernoulli policy.
             assert binomtest(int(counts[0]), T, (1 - p) ** n).pvalue > 1e-4
+
+
+def test_delay_step_waits_for_the_fastest():
+    """Sec. VI-B: the master continues with the n - s workers that finish first."""
+    n = 12
+    for s in range(n):
+        for t in range(50):
+            mask, delays, sec = R.delay_step(77, t, n, s, 1.5, 0.25)
+            finish = 0.25 + delays
+            assert mask.sum() == s and np.all(delays >= 0.0)
+            waited, skipped = finish[mask == 0], finish[mask == 1]
+            assert sec == waited.max()
+            if s:
+                assert skipped.min() >= waited.max()
+            # The master proceeds at the first instant when n - s have finished.
+            assert (finish <= sec).sum() >= n - s and (finish < sec).sum() < n - s
+            # The workers it skips are those of the slowest-draws policy.
+            assert np.array_equal(mask, R.straggler_mask(77, t, R.POLICY_SLOWEST, n, s))
+    mask, delays, sec = R.delay_step(77, 3, n, 0, 2.0, 1.0)
+    assert sec == 1.0 + delays.max() and mask.sum() == 0
+    mask, delays, sec = R.delay_step(77, 3, n, 4, 0.0, 1.0)
+    assert sec == 1.0 and np.all(delays == 0.0) and mask.sum() == 4
+
+
+@pytest.mark.parametrize("n,s,mean", [(12, 0, 1.0), (12, 1, 2.0), (12, 3, 1.0), (5, 4, 2.0)])
+def test_delay_step_matches_exponential_order_statistics(n, s, mean):
+    """The k-th smallest of n i.i.d. exponentials of mean mu has mean
+    mu * sum_{j<k} 1/(n - j) and variance mu^2 * sum_{j<k} 1/(n - j)^2
+    (Renyi's representation); k = n - s here."""
+    T = 6000
+    secs = np.array([R.delay_step(2024, t, n, s, mean)[2] for t in range(T)])
+    k = n - s
+    mu = mean * sum(1.0 / (n - j) for j in range(k))
+    sd = mean * math.sqrt(sum(1.0 / (n - j) ** 2 for j in range(k)))
+    assert abs(secs.mean() - mu) < 5.0 * sd / math.sqrt(T)
+    assert abs(secs.std() - sd) < 0.1 * sd
+
+
+def test_delays_are_exponential():
+    from scipy.stats import kstest
+    delays = np.concatenate([R.delay_step(5, t, 16, 0, 2.0)[1] for t in range(2000)])
+    assert kstest(delays, "expon", args=(0.0, 2.0)).pvalue > 1e-4
 
 
 def test_null_space_generator_entries():

@@ -29,6 +29,7 @@ import torch
 POLICY_EXACT = 0
 POLICY_UNIFORM_COUNT = 1
 POLICY_BERNOULLI = 2
+POLICY_SLOWEST = 3
 
 
 @dataclass(frozen=True)
