@@ -77,7 +77,7 @@ struct pgc_ctx {
   Grid head_warm, head_pipe;  // MLP head grids
   int64_t kpad = 0, m_pad = 0, pstride = 0;
   size_t off_ring = 0, off_coded = 0, off_decoded = 0, off_partials = 0, off_coef = 0, ws_need = 0;
-  size_t off_w1t = 0, off_w2t = 0, off_w2p = 0, off_h = 0, off_dz1t = 0;
+  size_t off_w1t = 0, off_w2t = 0, off_w2p = 0, off_h = 0, off_dz1 = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
@@ -138,7 +138,7 @@ void compute_layout(pgc_ctx* ctx) {
     ctx->off_w2t = take(2 * static_cast<size_t>(pgc::kMlpMaxClasses * hidden));
     ctx->off_w2p = take(2 * static_cast<size_t>(hidden * pgc::kMlpMaxClasses));
     ctx->off_h = take(2 * static_cast<size_t>(n) * ctx->m * hidden);
-    ctx->off_dz1t = take(2 * static_cast<size_t>(n) * hidden * ctx->m_pad);
+    ctx->off_dz1 = take(2 * static_cast<size_t>(n) * hidden * ctx->m_pad);
     ctx->off_partials = take(sizeof(float) * static_cast<size_t>(head_blocks * ctx->pstride));
   } else {
     const int64_t target = pgc::linear_grad_target_blocks(static_cast<int>(q));
@@ -516,7 +516,7 @@ int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::De
   __bf16* W2T = ws_ptr<__bf16>(ctx, ctx->off_w2t);
   __bf16* W2p = ws_ptr<__bf16>(ctx, ctx->off_w2p);
   __bf16* H = ws_ptr<__bf16>(ctx, ctx->off_h);
-  __bf16* dZ1T = ws_ptr<__bf16>(ctx, ctx->off_dz1t);
+  __bf16* dZ1 = ws_ptr<__bf16>(ctx, ctx->off_dz1);
   float* ring = ws_ptr<float>(ctx, ctx->off_ring);
   float* partials = ws_ptr<float>(ctx, ctx->off_partials);
 
@@ -539,7 +539,7 @@ int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::De
   hd.W2T = W2T;
   hd.W2p = W2p;
   hd.b2 = w + w1 + hidden + static_cast<int64_t>(hidden) * classes;
-  hd.dZ1T = dZ1T;
+  hd.dZ1 = dZ1;
   hd.partials = partials;
   hd.m = ctx->m;
   hd.m_pad = ctx->m_pad;
@@ -554,7 +554,7 @@ int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::De
   hd.pstride = static_cast<int32_t>(ctx->pstride);
   pgc::MlpWgradArgs wg{};
   wg.X = fw.X;
-  wg.dZ1T = dZ1T;
+  wg.dZ1 = dZ1;
   wg.ring = ring;
   wg.m = ctx->m;
   wg.m_pad = ctx->m_pad;

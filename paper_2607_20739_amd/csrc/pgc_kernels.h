@@ -119,9 +119,16 @@ struct MlpForwardArgs {
 };
 hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s);
 
+// dZ1 layout, blocked by 16 rows: element (r, h) of evaluated partition e at
+// dZ1[((e * m_pad / 16 + r / 16) * hidden + h) * 16 + r % 16], r < m_pad (a
+// multiple of 64; zero for r >= m).  A 16-row tile is one contiguous run, and
+// 8 consecutive rows of one hidden unit are 16 contiguous bytes.
+__host__ __device__ inline int64_t mlp_dz1_index(int64_t m_pad, int32_t hidden, int32_t e, int64_t r, int32_t h) {
+  return ((static_cast<int64_t>(e) * (m_pad / 16) + r / 16) * hidden + h) * 16 + r % 16;
+}
+
 // Per 16-row tile: logits, softmax, dZ2 = (p - onehot(y)) / m, dZ1 = (dZ2 W2^T)
-// masked by H > 0, written transposed to dZ1T[e][h][r] (r < m_pad, a multiple
-// of 64; zero for r >= m).  Each block writes partial sums of dW2^T[16][hidden], db1[hidden]
+// masked by H > 0, written to dZ1 in the blocked layout above.  Each block writes partial sums of dW2^T[16][hidden], db1[hidden]
 // and db2[16] to partials[(e * blocks_per_part + b) * pstride].
 struct MlpHeadArgs {
   const __bf16* H;
@@ -129,7 +136,7 @@ struct MlpHeadArgs {
   const __bf16* W2T;
   const __bf16* W2p;
   const float* b2;
-  __bf16* dZ1T;
+  __bf16* dZ1;
   float* partials;
   int64_t m, m_pad, rows_per_block;
   float inv_m;
@@ -138,11 +145,11 @@ struct MlpHeadArgs {
 int mlp_head_threads(int hidden);
 hipError_t launch_mlp_head(const MlpHeadArgs& a, hipStream_t s);
 
-// dW1[i][h] = sum_r X[k*m + r][i] dZ1T[e][h][r], written into the ring slot of
+// dW1[i][h] = sum_r X[k*m + r][i] dZ1(e; r, h), written into the ring slot of
 // partition k: ring[((plane * n + k) * ld) + i * hidden + h].
 struct MlpWgradArgs {
   const __bf16* X;
-  const __bf16* dZ1T;
+  const __bf16* dZ1;
   float* ring;
   int64_t m, m_pad, ld;
   int32_t d_in, hidden, n, plane, n_eval, part_stride, part_offset;

@@ -4,10 +4,10 @@
 //
 // Per step, for the evaluated partitions:
 //   cast     w (fp32) -> W1T, W2T, W2p (bf16 copies laid out for the MFMAs)
-//   forward  H = relu(X W1 + b1)                       MFMA 16x16x32, LDS-tiled,
-//            register prefetch, XCD-aware tile order
+//   forward  H = relu(X W1 + b1)                       MFMA 16x16x32, tiles loaded
+//            straight into swizzled LDS, XCD-aware tile order
 //   head     logits = H W2 + b2, softmax, dZ2 = (p - onehot) / m,
-//            dZ1 = (dZ2 W2^T) * [H > 0] (stored transposed), and block
+//            dZ1 = (dZ2 W2^T) * [H > 0] (16-row blocked), and block
 //            partials of dW2 = H^T dZ2, db1, db2         MFMA 16x16x32 / 16x16x16
 //   wgrad    dW1 = X^T dZ1 straight into the ring slot  MFMA 16x16x32, X tile
 //            transposed through LDS
@@ -70,28 +70,67 @@ void mlp_cast_w2_kernel(MlpCastArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// forward: H = relu(X W1 + b1).  Block tile 128 rows x 128 hidden, K step 64,
-// 4 waves as 2 x 2 (64 x 64 each) on 16x16x32 MFMAs, two blocks per CU.
-// Global tiles are fetched one K step ahead into registers and staged
-// through double-buffered LDS (one barrier per K step).  Block ids are mapped
-// so that all hidden tiles of a row tile run on the same XCD (workgroups are
-// dealt to the 8 XCDs round-robin) and share that XCD's L2 copy of X.
+// forward: H = relu(X W1 + b1).  Block tile 256 rows x 256 hidden, K step 32,
+// 8 waves as 2 (rows) x 4 (hidden), 128 x 64 each, one block per CU.  Tiles
+// travel from global memory straight into LDS (16 bytes per lane, no register
+// staging) through four buffers, three K steps ahead: one barrier per K step.
+// In a tile row of 32 bf16 (four 16-byte chunks) chunk ch of row r sits at
+// slot ch ^ (((r >> 1) ^ (r >> 2)) & 3): any 8 consecutive rows of a 16-row
+// fragment read fall on distinct 16-byte slots modulo 128 bytes, and all 16
+// modulo 256 bytes.  The MFMAs produce H^T (A = W1^T rows, B = X rows), which leaves four
+// consecutive hidden units of one sample in each lane: one 8-byte store.
+// Block ids are mapped so that all hidden tiles of a row tile run on the same
+// XCD (workgroups are dealt to the 8 XCDs round-robin) and share its L2.
 // ---------------------------------------------------------------------------
 
-constexpr int kFwBM = 128, kFwBN = 128, kFwBK = 64, kFwLd = kFwBK + 8;
+constexpr int kFwBM = 256, kFwBN = 256, kFwBK = 64, kFwStages = 2;
+static_assert(kFwBK == 32 || kFwBK == 64, "swizzle");
+constexpr int kFwThreads = 512;
+constexpr int kFwTile = kFwBM * kFwBK;          // bf16 per operand tile (32 KiB)
+constexpr int kFwRounds = kFwTile / 8 / kFwThreads;   // 16-byte chunks per thread per tile
 constexpr int kXcds = 8;
+static_assert(kFwBM == kFwBN, "one load pattern serves both operand tiles");
+static_assert(kFwStages * 2 * kFwTile >= kFwBM * kFwBN, "the output tile is staged in the operand buffers");
 
-struct FwStage {
-  bf16x8 a[4], b[4];
-};
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
 
-__global__ __launch_bounds__(256, 2)
+// 16 bytes from global memory to LDS: lane l of the wave writes lds_wave_base + 16 l.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+// Swizzle of a tile row's 16-byte chunks (an involution on 0 .. BK/8 - 1).
+__device__ __forceinline__ int fw_swizzle(int row) {
+  if constexpr (kFwBK == 32) return ((row >> 1) ^ (row >> 2)) & 3;
+  else return (row ^ (row >> 3)) & 7;
+}
+__device__ __forceinline__ int fw_slot(int row, int ch) { return row * kFwBK + ((ch ^ fw_swizzle(row)) << 3); }
+
+// Workgroup barrier without the memory fence of __syncthreads(), whose release
+// would wait for every outstanding load, prefetches included.  The callers
+// wait for the loads they need with wait_vmcnt; every LDS read before the
+// barrier has been consumed by then.  The empty asm statements keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt with vmcnt = n (n < 16) and the other counters left alone.
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(n >= 0 && n < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | n);
+}
+
+__global__ __launch_bounds__(kFwThreads, 1)
 void mlp_forward_kernel(MlpForwardArgs a) {
-  __shared__ bf16 As[2][kFwBM][kFwLd];
-  __shared__ bf16 Bs[2][kFwBN][kFwLd];
+  __shared__ __attribute__((aligned(16))) bf16 smem[kFwStages][2][kFwTile];   // [buffer][X, W1^T]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wr = wave >> 2, wh = wave & 3;
 
   const int htiles = a.hidden / kFwBN;
   const int64_t tiles_per_part = (a.m + kFwBM - 1) / kFwBM;
@@ -108,74 +147,104 @@ void mlp_forward_kernel(MlpForwardArgs a) {
   const bf16* Xp = a.X + part * a.m * a.d_in;
   const int ksteps = a.kpad / kFwBK;
   const int dchunks = a.d_in / 8;
+  constexpr int kCpr = kFwBK / 8;   // 16-byte chunks per tile row
 
-  auto fetch = [&](FwStage& st, int ks) {
+  // Chunk c = u * 512 + tid of a tile is row c / kCpr at slot c % kCpr, which
+  // holds the logical chunk given by the swizzle (an involution).  Rows past the partition read its last
+  // row, chunks past d_in read the row's first chunk: both are finite values
+  // that meet zero weights or land in rows that are never stored.
+  int64_t xoff[kFwRounds];
+  int32_t woff[kFwRounds], chunk[kFwRounds];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + u * 256, row = idx >> 3, ch = idx & 7;
-      const int kc = ks * 8 + ch;
-      const int64_t gr = r0 + row;
-      st.a[u] = (gr < a.m && kc < dchunks) ? load_vec<bf16x8>(Xp + gr * a.d_in + kc * 8) : bf16x8{};
-      st.b[u] = load_vec<bf16x8>(a.W1T + static_cast<int64_t>(h0 + row) * a.kpad + ks * kFwBK + ch * 8);
+  for (int u = 0; u < kFwRounds; ++u) {
+    const int c = u * kFwThreads + tid, row = c / kCpr;
+    chunk[u] = (c % kCpr) ^ fw_swizzle(row);
+    xoff[u] = static_cast<int64_t>(r0 + row < a.m ? r0 + row : a.m - 1) * a.d_in;
+    woff[u] = (h0 + row) * a.kpad;
+  }
+  auto issue = [&](int ks, int buf) {
+#pragma unroll
+    for (int u = 0; u < kFwRounds; ++u) {
+      const int kc = ks * kCpr + chunk[u];
+      const int dst = (u * kFwThreads + wave * 64) * 8;
+      load_lds16(Xp + xoff[u] + (kc < dchunks ? kc * 8 : 0), &smem[buf][0][dst]);
+      load_lds16(a.W1T + woff[u] + kc * 8, &smem[buf][1][dst]);
     }
   };
-  auto stage = [&](const FwStage& st, int buf) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + u * 256, row = idx >> 3, ch = idx & 7;
-      *reinterpret_cast<bf16x8*>(&As[buf][row][ch * 8]) = st.a[u];
-      *reinterpret_cast<bf16x8*>(&Bs[buf][row][ch * 8]) = st.b[u];
-    }
-  };
 
-  f32x4 acc[4][4];
+  f32x4 acc[4][8];   // [hidden tile][sample tile], D = H^T
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x4{};
+    for (int mt = 0; mt < 8; ++mt) acc[nt][mt] = f32x4{};
   auto compute = [&](int buf) {
+    const bf16* Xs = smem[buf][0];
+    const bf16* Ws = smem[buf][1];
 #pragma unroll
     for (int kk = 0; kk < kFwBK / 32; ++kk) {
-      bf16x8 af[4], bfr[4];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        af[mt] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * 64 + mt * 16 + lr][kk * 32 + lg * 8]);
+      const int ch = kk * 4 + lg;
+      bf16x8 wf[4], xf[8];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
-        bfr[nt] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * 64 + nt * 16 + lr][kk * 32 + lg * 8]);
+        wf[nt] = *reinterpret_cast<const bf16x8*>(&Ws[fw_slot(wh * 64 + nt * 16 + lr, ch)]);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int mt = 0; mt < 8; ++mt)
+        xf[mt] = *reinterpret_cast<const bf16x8*>(&Xs[fw_slot(wr * 128 + mt * 16 + lr, ch)]);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma_k32(af[mt], bfr[nt], acc[mt][nt]);
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) acc[nt][mt] = mfma_k32(wf[nt], xf[mt], acc[nt][mt]);
     }
   };
 
-  // Invariant at the top of step ks: LDS buffer ks % 2 holds step ks and the
-  // registers s0 hold step ks + 1.
-  FwStage s0;
-  fetch(s0, 0);
-  stage(s0, 0);
-  __syncthreads();
-  if (1 < ksteps) fetch(s0, 1);
+  // Each issue() is 2 * kFwRounds loads per lane.  At the top of step ks the
+  // steps after ks already issued are min(kFwStages - 2, ksteps - 1 - ks).
+  constexpr int kLoads = 2 * kFwRounds;
+  static_assert(kFwStages >= 2 && kFwStages <= 4 && (kFwStages - 2) * kLoads < 16, "vmcnt field");
+#pragma unroll
+  for (int p = 0; p < kFwStages - 1; ++p)
+    if (p < ksteps) issue(p, p);
   for (int ks = 0; ks < ksteps; ++ks) {
-    compute(ks & 1);
-    if (ks + 1 < ksteps) stage(s0, (ks + 1) & 1);
-    __syncthreads();
-    if (ks + 2 < ksteps) fetch(s0, ks + 2);
+    // This wave's loads of step ks have landed; after the barrier every
+    // wave's have, and every wave is done reading buffer (ks - 1) % 4.
+    const int later = min(kFwStages - 2, ksteps - 1 - ks);
+    if (later >= 2) wait_vmcnt<(kFwStages >= 4 ? 2 * kLoads : 0)>();
+    else if (later == 1) wait_vmcnt<(kFwStages >= 3 ? kLoads : 0)>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (ks + kFwStages - 1 < ksteps) issue(ks + kFwStages - 1, (ks + kFwStages - 1) % kFwStages);
+    compute(ks % kFwStages);
   }
 
-  bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * a.hidden;
+  // Epilogue: bias and ReLU, then the 256 x 256 bf16 tile goes through LDS
+  // (row r's 16-byte chunk cc at slot cc ^ (r & 31)) so that H leaves in whole
+  // 512-byte row segments, 16 bytes per lane.
+  lds_barrier();   // every wave is done reading the operand buffers
+  bf16* out = &smem[0][0][0];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
-    const int h = h0 + wn * 64 + nt * 16 + lr;
-    const float bias = a.b1[h];
+    const int hl = wh * 64 + nt * 16 + lg * 4;   // hidden column within the tile
+    float bias[4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int i = 0; i < 4; ++i) bias[i] = a.b1[h0 + hl + i];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t row = r0 + wm * 64 + mt * 16 + lg * 4 + i;
-        if (row < a.m) Hp[row * a.hidden + h] = static_cast<bf16>(fmaxf(acc[mt][nt][i] + bias, 0.0f));
-      }
+    for (int mt = 0; mt < 8; ++mt) {
+      const int r = wr * 128 + mt * 16 + lr;
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = static_cast<bf16>(fmaxf(acc[nt][mt][i] + bias[i], 0.0f));
+      *reinterpret_cast<bf16x4*>(&out[r * kFwBN + (((hl >> 3) ^ (r & 31)) << 3) + (hl & 4)]) = v;
+    }
+  }
+  lds_barrier();
+  bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * a.hidden + h0;
+  const int cc = tid & 31;
+#pragma unroll 4
+  for (int r = tid >> 5; r < kFwBM; r += kFwThreads / 32) {
+    const int64_t row = r0 + r;
+    if (row < a.m)
+      *reinterpret_cast<bf16x8*>(Hp + row * a.hidden + cc * 8) =
+          *reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)]);
   }
 }
 
@@ -183,14 +252,14 @@ void mlp_forward_kernel(MlpForwardArgs a) {
 // head: one wave per 128 hidden columns, 16-row tiles.  The wave's partial
 // logits are summed across waves through LDS in wave order (one barrier per
 // tile).  Each wave stages its 16 x 128 tile of H and of dZ1 through its own
-// LDS area: the ReLU mask and the dW2 operand are read from there, and dZ1^T
-// leaves in 16-byte row-contiguous stores.
+// LDS area: the ReLU mask and the dW2 operand are read from there, and the
+// tile's dZ1 leaves as one contiguous 4 KiB run per wave (16-row blocked layout).
 // ---------------------------------------------------------------------------
 
 constexpr int kHeadCols = 128;
 constexpr int kHeadMaxWaves = kMlpMaxHidden / kHeadCols;
 constexpr int kHtLd = kHeadCols + 8;   // H tile row stride (bf16)
-constexpr int kZtLd = 16 + 8;          // dZ1^T tile row stride (bf16)
+constexpr int kZtLd = 16 + 8;          // dZ1 tile stride per hidden unit (bf16)
 
 __global__ __launch_bounds__(64 * kHeadMaxWaves)
 void mlp_head_kernel(MlpHeadArgs a) {
@@ -207,7 +276,7 @@ void mlp_head_kernel(MlpHeadArgs a) {
   const int64_t hidden = a.hidden;
   const bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * hidden;
   const int32_t* yp = a.y + part * a.m;
-  bf16* dz1 = a.dZ1T + static_cast<int64_t>(e) * hidden * a.m_pad;
+  bf16* dz1 = a.dZ1 + mlp_dz1_index(a.m_pad, a.hidden, e, 0, 0);
   const int64_t rbeg = static_cast<int64_t>(blockIdx.x) * a.rows_per_block;
   const int64_t rend = min(rbeg + a.rows_per_block, a.m_pad);
 
@@ -299,11 +368,11 @@ void mlp_head_kernel(MlpHeadArgs a) {
       for (int j = 0; j < 4; ++j) hb[j] = Ht[wave][lg * 4 + j][h + lr];
       dw2[ht] = mfma_k16(dz_a, hb, dw2[ht]);
     }
-    // dZ1^T rows: lane writes 8 consecutive rows of column hw0 + lane/2 + 32 k.
+    // dZ1 block of rows r0 .. r0 + 15: lane writes 8 rows of hidden unit hw0 + lane/2 + 32 k.
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int hl = lane / 2 + 32 * k, half = lane & 1;
-      *reinterpret_cast<bf16x8*>(dz1 + static_cast<int64_t>(hw0 + hl) * a.m_pad + r0 + half * 8) =
+      *reinterpret_cast<bf16x8*>(dz1 + ((r0 / 16) * hidden + hw0 + hl) * 16 + half * 8) =
           *reinterpret_cast<const bf16x8*>(&Zt[wave][hl][half * 8]);
     }
   }
@@ -331,8 +400,9 @@ void mlp_head_kernel(MlpHeadArgs a) {
 
 // ---------------------------------------------------------------------------
 // wgrad: dW1^T tile 256 hidden x 112 features per block, K = rows in steps of
-// 64; 4 waves, each 64 hidden x 112 features.  dZ1T rows feed the A operand
-// straight from global memory; the X tile is transposed into LDS as 32-bit
+// 64; 4 waves, each 64 hidden x 112 features.  dZ1 (16-row blocked, so 8
+// rows of a hidden unit are 16 contiguous bytes) feeds the A operand straight
+// from global memory; the X tile is transposed into LDS as 32-bit
 // words holding two consecutive rows of one feature.  The staging lanes of a
 // wave cover 32 row pairs x 2 feature chunks, so with a row stride of 36
 // words each of its stores touches 64 distinct banks, and the B-operand reads
@@ -348,12 +418,27 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   __shared__ bf16 XT[2][kWgBN][kWgLd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int e = blockIdx.z;
+  // With at least 8 evaluated partitions, every tile of a partition goes to
+  // the same XCD (workgroups are dealt to the 8 XCDs round-robin), so its L2
+  // serves the dZ1 rows to all feature tiles and the X rows to all hidden
+  // tiles; otherwise the tiles are spread over the chip.
+  const int htiles = a.hidden / kWgBM, ftiles = (a.d_in + kWgBN - 1) / kWgBN;
+  const int tiles = htiles * ftiles;
+  int e, tile;
+  if (a.n_eval >= kXcds) {
+    const int local = static_cast<int>(blockIdx.x) / kXcds;
+    e = (local / tiles) * kXcds + static_cast<int>(blockIdx.x) % kXcds;
+    tile = local % tiles;
+    if (e >= a.n_eval) return;
+  } else {
+    e = static_cast<int>(blockIdx.x) / tiles;
+    tile = static_cast<int>(blockIdx.x) % tiles;
+  }
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
-  const int hb0 = blockIdx.x * kWgBM + wave * 64;
-  const int i0 = blockIdx.y * kWgBN;
+  const int hb0 = (tile % htiles) * kWgBM + wave * 64;
+  const int i0 = (tile / htiles) * kWgBN;
   const bf16* Xp = a.X + part * a.m * a.d_in;
-  const bf16* dz = a.dZ1T + static_cast<int64_t>(e) * a.hidden * a.m_pad;
+  const bf16* dz = a.dZ1 + mlp_dz1_index(a.m_pad, a.hidden, e, 0, 0);
   const int ksteps = static_cast<int>(a.m_pad / kWgBK);
   const int dchunks = a.d_in / 8;
 
@@ -395,8 +480,8 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
-        av[mt][kk] = load_vec<bf16x8>(dz + static_cast<int64_t>(hb0 + mt * 16 + lr) * a.m_pad +
-                                      ks * kWgBK + kk * 32 + lg * 8);
+        av[mt][kk] = load_vec<bf16x8>(dz + mlp_dz1_index(a.m_pad, a.hidden, 0, ks * kWgBK + kk * 32 + lg * 8,
+                                                         hb0 + mt * 16 + lr));
   };
 
   f32x4 acc[4][7];
@@ -486,7 +571,7 @@ hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s) {
 hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s) {
   const int64_t rtiles = (a.m + kFwBM - 1) / kFwBM * a.n_eval;
   dim3 grid(static_cast<unsigned>((rtiles + kXcds - 1) / kXcds * kXcds * (a.hidden / kFwBN)));
-  hipLaunchKernelGGL(mlp_forward_kernel, grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL(mlp_forward_kernel, grid, dim3(kFwThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -499,7 +584,9 @@ hipError_t launch_mlp_head(const MlpHeadArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_mlp_wgrad(const MlpWgradArgs& a, hipStream_t s) {
-  dim3 grid(a.hidden / kWgBM, (a.d_in + kWgBN - 1) / kWgBN, a.n_eval);
+  const int tiles = (a.hidden / kWgBM) * ((a.d_in + kWgBN - 1) / kWgBN);
+  const int parts = a.n_eval >= kXcds ? (a.n_eval + kXcds - 1) / kXcds * kXcds : a.n_eval;
+  dim3 grid(static_cast<unsigned>(tiles * parts));
   hipLaunchKernelGGL(mlp_wgrad_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
