@@ -9,8 +9,8 @@
 //   head     logits = H W2 + b2, softmax, dZ2 = (p - onehot) / m,
 //            dZ1 = (dZ2 W2^T) * [H > 0] (16-row blocked), and block
 //            partials of dW2 = H^T dZ2, db1, db2         MFMA 16x16x32 / 16x16x16
-//   wgrad    dW1 = X^T dZ1 straight into the ring slot  MFMA 16x16x32, X tile
-//            transposed through LDS
+//   wgrad    dW1 = X^T dZ1 straight into the ring slot  MFMA 16x16x32, both tiles
+//            loaded straight into LDS, X fragments by transposing LDS reads
 //   reduce   head partials -> b1, W2, b2 parts of the ring slot (fp64, fixed order)
 //
 // MFMA lane layouts (gfx950, wave64; l = lane, lr = l % 16, lg = l / 16):
@@ -399,25 +399,60 @@ void mlp_head_kernel(MlpHeadArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// wgrad: dW1^T tile 256 hidden x 112 features per block, K = rows in steps of
-// 64; 4 waves, each 64 hidden x 112 features.  dZ1 (16-row blocked, so 8
-// rows of a hidden unit are 16 contiguous bytes) feeds the A operand straight
-// from global memory; the X tile is transposed into LDS as 32-bit
-// words holding two consecutive rows of one feature.  The staging lanes of a
-// wave cover 32 row pairs x 2 feature chunks, so with a row stride of 36
-// words each of its stores touches 64 distinct banks, and the B-operand reads
-// (16 rows x 16 bytes) are conflict-free as well.
+// wgrad: dW1^T = dZ1^T X per partition, block tile 256 hidden x 112 features,
+// K = rows in steps of 64.  8 waves: wave (wh, wk) owns hidden rows
+// 64 wh .. 64 wh + 63 and the rows 32 wk .. 32 wk + 31 of every K step; the
+// two K halves are added through LDS at the end (fixed order).  Both operands
+// travel from global memory straight into LDS, two K steps ahead, through
+// three buffers (every load in the loop is such a load, so they complete in
+// order and the per-step waits count them exactly):
+//   A (dZ1, 16-row blocked): [4 row blocks][256 hidden][2 halves of 8 rows],
+//     half s of hidden h stored at s ^ (((h >> 2) ^ (h >> 3)) & 1); the
+//     fragments are plain 16-byte reads.
+//   B (X rows): [64 rows][16 chunks of 16 bytes], the tile's 14 feature
+//     chunks plus 2 spare, chunk j of row r at slot j ^ g(r) with g(r) even
+//     and distinct over rows {0..3, 8..11}, so that the 32-byte row pieces a
+//     transposing read gathers spread over the banks.  The fragments (8 rows
+//     of one feature per lane) come from two transposing 8-byte reads: within
+//     each 16-lane group, lane i receives element i % 4 of the 4-element row
+//     pieces addressed by lanes 4 j + i / 4, j = 0..3.
 // ---------------------------------------------------------------------------
 
-constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 64, kWgLd = kWgBK + 8;
-constexpr int kWgPairs = kWgBK / 2;                   // row pairs per K step
-constexpr int kWgItems = kWgPairs * (kWgBN / 8);      // (row pair, feature chunk) items
+constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 64, kWgStages = 3;
+constexpr int kWgThreads = 512;
+constexpr int kWgAChunks = kWgBM * kWgBK / 8;          // 16-byte chunks of an A stage (2048)
+constexpr int kWgBRowChunks = kWgBN / 8;               // 14 per X row ...
+constexpr int kWgBRowSlots = 16;                       // ... in 16 slots
+constexpr int kWgBChunks = kWgBK * kWgBRowSlots;       // 1024
+constexpr int kWgStageBytes = (kWgAChunks + kWgBChunks) * 16;
+constexpr int kWgALoads = kWgAChunks / kWgThreads, kWgBLoads = kWgBChunks / kWgThreads;
+static_assert(kWgALoads * kWgThreads == kWgAChunks && kWgBLoads * kWgThreads == kWgBChunks, "load rounds");
+static_assert(kWgStages * kWgStageBytes <= 160 * 1024, "LDS");
+static_assert(4 * 28 * 64 * 16 <= kWgStages * kWgStageBytes, "the K-half reduction fits the stages");
 
-__global__ __launch_bounds__(256)
+typedef bf16 bf16x4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4v lds_bf16x4;
+
+__device__ __forceinline__ int wg_half_swizzle(int h) { return ((h >> 2) ^ (h >> 3)) & 1; }
+__device__ __forceinline__ int wg_row_swizzle(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
+
+// Transposing 8-byte LDS read, issued as inline assembly: for the builtin the
+// compiler waits for every outstanding direct-to-LDS load first (it cannot
+// tell the buffers apart), which would drain the prefetch.  The kernel's own
+// waits and barrier order the loads; the caller waits for lgkmcnt before use.
+__device__ __forceinline__ bf16x4v ds_read_tr16(const bf16* p) {
+  bf16x4v v;
+  const uint32_t addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_bf16x4*)p));
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
+__global__ __launch_bounds__(kWgThreads, 1)
 void mlp_wgrad_kernel(MlpWgradArgs a) {
-  __shared__ bf16 XT[2][kWgBN][kWgLd];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kWgStages * kWgStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
+  const int wh = wave & 3, wk = wave >> 2;
   // With at least 8 evaluated partitions, every tile of a partition goes to
   // the same XCD (workgroups are dealt to the 8 XCDs round-robin), so its L2
   // serves the dZ1 rows to all feature tiles and the X rows to all hidden
@@ -435,53 +470,46 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
     tile = static_cast<int>(blockIdx.x) % tiles;
   }
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
-  const int hb0 = (tile % htiles) * kWgBM + wave * 64;
+  const int hb0 = (tile % htiles) * kWgBM;
   const int i0 = (tile / htiles) * kWgBN;
   const bf16* Xp = a.X + part * a.m * a.d_in;
   const bf16* dz = a.dZ1 + mlp_dz1_index(a.m_pad, a.hidden, e, 0, 0);
   const int ksteps = static_cast<int>(a.m_pad / kWgBK);
-  const int dchunks = a.d_in / 8;
 
-  // Staging items t and t + 256: row pair rp = item % 32, feature chunk fc = item / 32.
-  bf16x8 x[2][2];
-  auto fetch_x = [&](int ks) {
+  // A chunk c = u * 512 + tid: row block c / 512, hidden (c % 512) / 2, slot
+  // c % 2 holding half (c % 2) ^ swizzle; its source is that half of the row
+  // block of dZ1 (a run of 8 KiB per row block in global memory).
+  int32_t aoff[kWgALoads];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int item = tid + u * 256;
-      x[u][0] = bf16x8{};
-      x[u][1] = bf16x8{};
-      if (item >= kWgItems) continue;
-      const int rp = item % kWgPairs, fc = item / kWgPairs;
-      if (i0 / 8 + fc >= dchunks) continue;
-      const int64_t r = static_cast<int64_t>(ks) * kWgBK + 2 * rp;
-      if (r < a.m) x[u][0] = load_vec<bf16x8>(Xp + r * a.d_in + i0 + fc * 8);
-      if (r + 1 < a.m) x[u][1] = load_vec<bf16x8>(Xp + (r + 1) * a.d_in + i0 + fc * 8);
+  for (int u = 0; u < kWgALoads; ++u) {
+    const int c = u * kWgThreads + tid, rb = c >> 9, h = (c & 511) >> 1;
+    aoff[u] = (rb * a.hidden + hb0 + h) * 16 + ((c & 1) ^ wg_half_swizzle(h)) * 8;
+  }
+  // B chunk c: row c / 16 at slot c % 16, holding feature chunk
+  // j = (c % 16) ^ g(row).  Spare chunks (j >= 14) and chunks past d_in read
+  // the tile's first chunk of the row; a row past the partition reads its last
+  // row: all meet zeros or land in columns that are never used or stored.
+  int32_t brow[kWgBLoads], bcol[kWgBLoads];
+#pragma unroll
+  for (int u = 0; u < kWgBLoads; ++u) {
+    const int c = u * kWgThreads + tid, row = c / kWgBRowSlots;
+    const int j = (c % kWgBRowSlots) ^ wg_row_swizzle(row);
+    const int col = i0 + j * 8;
+    brow[u] = row;
+    bcol[u] = (j < kWgBRowChunks && col < a.d_in) ? col : i0;
+  }
+  auto stage_a = [&](int buf) { return reinterpret_cast<bf16*>(smem + buf * kWgStageBytes); };
+  auto stage_b = [&](int buf) { return reinterpret_cast<bf16*>(smem + buf * kWgStageBytes + kWgAChunks * 16); };
+  auto issue = [&](int ks, int buf) {
+    const bf16* dzk = dz + static_cast<int64_t>(ks) * (kWgBK / 16) * a.hidden * 16;
+#pragma unroll
+    for (int u = 0; u < kWgALoads; ++u)
+      load_lds16(dzk + aoff[u], stage_a(buf) + (u * kWgThreads + wave * 64) * 8);
+#pragma unroll
+    for (int u = 0; u < kWgBLoads; ++u) {
+      const int64_t r = static_cast<int64_t>(ks) * kWgBK + brow[u];
+      load_lds16(Xp + (r < a.m ? r : a.m - 1) * a.d_in + bcol[u], stage_b(buf) + (u * kWgThreads + wave * 64) * 8);
     }
-  };
-  auto stage_x = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int item = tid + u * 256;
-      if (item >= kWgItems) continue;
-      const int rp = item % kWgPairs, fc = item / kWgPairs;
-#pragma unroll
-      for (int f = 0; f < 8; ++f) {
-        typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
-        bf16x2 pair;
-        pair[0] = x[u][0][f];
-        pair[1] = x[u][1][f];
-        *reinterpret_cast<bf16x2*>(&XT[buf][fc * 8 + f][2 * rp]) = pair;
-      }
-    }
-  };
-  bf16x8 av[4][2];
-  auto fetch_a = [&](int ks) {
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-        av[mt][kk] = load_vec<bf16x8>(dz + mlp_dz1_index(a.m_pad, a.hidden, 0, ks * kWgBK + kk * 32 + lg * 8,
-                                                         hb0 + mt * 16 + lr));
   };
 
   f32x4 acc[4][7];
@@ -489,44 +517,76 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int nt = 0; nt < 7; ++nt) acc[mt][nt] = f32x4{};
-
-  fetch_x(0);
-  stage_x(0);
-  fetch_a(0);
-  __syncthreads();
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int buf = ks & 1;
-    bf16x8 af[4][2];
+  auto compute = [&](int buf) {
+    const bf16* As = stage_a(buf);
+    const bf16* Bs = stage_b(buf);
+    const int row = wk * 32 + lg * 8 + (lr >> 2);
+    // Feature 16 nt + 4 (lr & 3) .. + 3 sits in chunk 2 nt + ((lr & 3) >> 1), half (lr & 1).
+    auto bpos = [&](int r, int nt) {
+      return (r * kWgBRowSlots + ((2 * nt + ((lr & 3) >> 1)) ^ wg_row_swizzle(r))) * 8 + (lr & 1) * 4;
+    };
+    bf16x4v lo[7], hi[7];
+#pragma unroll
+    for (int nt = 0; nt < 7; ++nt) {
+      lo[nt] = ds_read_tr16(&Bs[bpos(row, nt)]);
+      hi[nt] = ds_read_tr16(&Bs[bpos(row + 4, nt)]);
+    }
+    const int rb = wk * 2 + (lg >> 1), half = lg & 1;
+    bf16x8 af[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      af[mt][0] = av[mt][0];
-      af[mt][1] = av[mt][1];
+      const int h = wh * 64 + mt * 16 + lr;
+      af[mt] = *reinterpret_cast<const bf16x8*>(&As[((rb * kWgBM + h) * 2 + (half ^ wg_half_swizzle(h))) * 8]);
     }
-    if (ks + 1 < ksteps) {
-      fetch_x(ks + 1);
-      fetch_a(ks + 1);
+    // The transposing reads are invisible to the compiler's wait insertion:
+    // wait here, with every result tied to the wait so no use moves above it.
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(lo[4]), "+v"(lo[5]), "+v"(lo[6]),
+                   "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]), "+v"(hi[4]), "+v"(hi[5]), "+v"(hi[6]));
+#pragma unroll
+    for (int nt = 0; nt < 7; ++nt) {
+      const bf16x8 bv = {lo[nt][0], lo[nt][1], lo[nt][2], lo[nt][3], hi[nt][0], hi[nt][1], hi[nt][2], hi[nt][3]};
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt], bv, acc[mt][nt]);
     }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int nt = 0; nt < 7; ++nt) {
-        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&XT[buf][nt * 16 + lr][kk * 32 + lg * 8]);
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt][kk], bv, acc[mt][nt]);
-      }
-    if (ks + 1 < ksteps) stage_x(buf ^ 1);
-    __syncthreads();
+  };
+
+  constexpr int kLoads = kWgALoads + kWgBLoads;
+  issue(0, 0);
+  if (1 < ksteps) issue(1, 1);
+  for (int ks = 0; ks < ksteps; ++ks) {
+    // This wave's loads of step ks have landed (step ks + 1's may still be in
+    // flight); after the barrier every wave's have, and every wave is done
+    // reading buffer (ks + 2) % 3, last used at step ks - 1.
+    if (ks + 1 < ksteps) wait_vmcnt<kLoads>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (ks + 2 < ksteps) issue(ks + 2, (ks + 2) % kWgStages);
+    compute(ks % kWgStages);
   }
 
+  // Add the two K halves: wk = 1 hands its sums to wk = 0 through LDS.
+  lds_barrier();
+  f32x4* red = reinterpret_cast<f32x4*>(smem) + wh * 28 * 64;
+  if (wk == 1) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < 7; ++nt) red[(mt * 7 + nt) * 64 + lane] = acc[mt][nt];
+  }
+  __syncthreads();
+  if (wk == 1) return;
   float* slot = a.ring + (static_cast<int64_t>(a.plane) * a.n + part) * a.ld;
 #pragma unroll
   for (int nt = 0; nt < 7; ++nt) {
     const int feat = i0 + nt * 16 + lr;
     if (feat >= a.d_in) continue;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-      *reinterpret_cast<f32x4*>(slot + static_cast<int64_t>(feat) * a.hidden + hb0 + mt * 16 + lg * 4) =
-          acc[mt][nt];
+    for (int mt = 0; mt < 4; ++mt) {
+      const f32x4 other = red[(mt * 7 + nt) * 64 + lane];
+      *reinterpret_cast<f32x4*>(slot + static_cast<int64_t>(feat) * a.hidden + hb0 + wh * 64 + mt * 16 + lg * 4) =
+          acc[mt][nt] + other;
+    }
   }
 }
 
@@ -587,7 +647,7 @@ hipError_t launch_mlp_wgrad(const MlpWgradArgs& a, hipStream_t s) {
   const int tiles = (a.hidden / kWgBM) * ((a.d_in + kWgBN - 1) / kWgBN);
   const int parts = a.n_eval >= kXcds ? (a.n_eval + kXcds - 1) / kXcds * kXcds : a.n_eval;
   dim3 grid(static_cast<unsigned>(tiles * parts));
-  hipLaunchKernelGGL(mlp_wgrad_kernel, grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL(mlp_wgrad_kernel, grid, dim3(kWgThreads), 0, s, a);
   return hipGetLastError();
 }
 
