@@ -18,7 +18,7 @@ import torch
 import paper_2607_20739_amd as P
 from oracle import pgc_oracle as O
 from workloads import WORKLOADS, Workload, make_inputs, POLICY_BERNOULLI, POLICY_EXACT, \
-    POLICY_UNIFORM_COUNT
+    POLICY_SLOWEST, POLICY_UNIFORM_COUNT
 
 from _parity import FP32_TOL, gpu_masks, gpu_run, gpu_session, normwise_error, oracle_masks, \
     oracle_run
@@ -133,6 +133,17 @@ BASELINES = [
               policy=POLICY_UNIFORM_COUNT, cap=11, seed=44), True),
     (Workload("is_sgd_mlp", "IS_SGD", "mlp", n=4, c=1, N=4 * 64, d=64, lr=0.05, steps=5,
               policy=POLICY_EXACT, cap=2, seed=45, hidden=256, classes=10), True),
+    # the delay model's stragglers: the s workers with the largest delay draws
+    (Workload("delay_cr_logistic_n12_c3", "CR", "logistic", n=12, c=3, N=12 * 256, d=768, lr=0.1, steps=10,
+              policy=POLICY_SLOWEST, cap=2, seed=46), True),
+    (Workload("delay_fr_lsq_n12_c4", "FR", "lsq", n=12, c=4, N=12 * 300, d=512, lr=0.05, steps=10,
+              policy=POLICY_SLOWEST, cap=3, seed=47), True),
+    # (naive real-valued CR at c = 6 needs decoding coefficients near 2e5, which
+    # multiply fp32 rounding past any fp32 bar; c = 3 peaks near 300)
+    (Workload("delay_real_logistic_n12_c3", "CR_REAL", "logistic", n=12, c=3, N=12 * 128, d=256, lr=0.05,
+              steps=8, policy=POLICY_SLOWEST, cap=2, seed=48, code_seed=7), True),
+    (Workload("delay_gc_real_lsq_n12_c3", "CR_REAL", "lsq", n=12, c=3, N=12 * 200, d=256, lr=0.02, steps=8,
+              policy=POLICY_SLOWEST, cap=2, seed=49, code_seed=7), False),
 ]
 
 
