@@ -107,13 +107,15 @@ __device__ __forceinline__ int fw_swizzle(int row) {
 }
 __device__ __forceinline__ int fw_slot(int row, int ch) { return row * kFwBK + ((ch ^ fw_swizzle(row)) << 3); }
 
-// Workgroup barrier without the memory fence of __syncthreads(), whose release
-// would wait for every outstanding load, prefetches included.  The callers
-// wait for the loads they need with wait_vmcnt; every LDS read before the
-// barrier has been consumed by then.  The empty asm statements keep the
-// compiler from moving memory accesses across it.
+// Workgroup barrier that orders LDS only: the wave's own LDS reads and writes
+// complete (lgkmcnt 0) before it, but outstanding global loads and stores do
+// not have to, unlike the release fence of __syncthreads(), which would drain
+// every prefetch.  Callers wait for the global loads they need with
+// wait_vmcnt.  The empty asm statements keep the compiler from moving memory
+// accesses across it.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63 (no wait), expcnt 7, lgkmcnt 0
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -298,27 +300,45 @@ void mlp_head_kernel(MlpHeadArgs a) {
   }
   float db2 = 0.0f;
   int buf = 0;
-  // H fragments of the logits GEMM (row r0 + lr, columns hw0 + 32 ks + 8 lg ..),
-  // fetched one tile ahead.
-  bf16x8 hnext[4];
-  auto fetch_h = [&](int64_t r0) {
+  // H fragments of the logits GEMM (row r0 + lr, columns hw0 + 32 ks + 8 lg ..)
+  // and the labels of rows r0 + 4 lg + i, fetched two tiles ahead into two
+  // alternating register sets (labels loaded later would make every wait for
+  // them wait for the prefetched tiles too: loads complete in order).
+  bf16x8 ha[4], hb[4];
+  int la[4], lb[4];
+  // Every fetch issues the same loads on every path (rows past the partition
+  // load its last row), and the values are only masked where a tile uses them,
+  // so the compiler's waits for a register set count exactly the loads issued
+  // after it.
+  auto fetch_h = [&](int64_t r0, bf16x8* dst, int* lab) {
     const int64_t row = r0 + lr;
+    const int64_t src = row < a.m ? row : a.m - 1;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      hnext[ks] = row < a.m ? load_vec<bf16x8>(Hp + row * hidden + hw0 + ks * 32 + lg * 8) : bf16x8{};
+    for (int ks = 0; ks < 4; ++ks) dst[ks] = load_vec<bf16x8>(Hp + src * hidden + hw0 + ks * 32 + lg * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t lrow = r0 + lg * 4 + i;
+      lab[i] = yp[lrow < a.m ? lrow : a.m - 1];
+    }
   };
-  if (rbeg < rend) fetch_h(rbeg);
-  for (int64_t r0 = rbeg; r0 < rend; r0 += 16) {
+  auto tile = [&](int64_t r0, bf16x8* hcur, int* lcur) {
     f32x4 z = f32x4{};
+    const bool hrow = r0 + lr < a.m;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      z = mfma_k32(hnext[ks], w2t[ks], z);
-      *reinterpret_cast<bf16x8*>(&Ht[wave][lr][ks * 32 + lg * 8]) = hnext[ks];
+      const bf16x8 hv = hrow ? hcur[ks] : bf16x8{};
+      z = mfma_k32(hv, w2t[ks], z);
+      *reinterpret_cast<bf16x8*>(&Ht[wave][lr][ks * 32 + lg * 8]) = hv;
     }
-    if (r0 + 16 < rend) fetch_h(r0 + 16);
+    int label[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) label[i] = r0 + lg * 4 + i < a.m ? lcur[i] : -1;
+    // The last two tiles of the block refetch themselves; the values go unused.
+    fetch_h(r0 + 32 < rend ? r0 + 32 : r0, hcur, lcur);
 #pragma unroll
     for (int i = 0; i < 4; ++i) zpart[buf][wave][lg * 4 + i][lr] = z[i];
-    __syncthreads();
+    // LDS-only barrier: the H prefetch and the dZ1 stores stay in flight.
+    lds_barrier();
     // Softmax over the classes of rows r0 + 4 lg + i (class lr on this lane).
     float dz2[4];
 #pragma unroll
@@ -335,8 +355,7 @@ void mlp_head_kernel(MlpHeadArgs a) {
       float sum = ex;
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
-      const int label = row < a.m ? yp[row] : -1;
-      dz2[i] = (row < a.m && live) ? (ex / sum - (lr == label ? 1.0f : 0.0f)) * a.inv_m : 0.0f;
+      dz2[i] = (row < a.m && live) ? (ex / sum - (lr == label[i] ? 1.0f : 0.0f)) * a.inv_m : 0.0f;
       db2 += dz2[i];
     }
     buf ^= 1;
@@ -375,6 +394,15 @@ void mlp_head_kernel(MlpHeadArgs a) {
       *reinterpret_cast<bf16x8*>(dz1 + ((r0 / 16) * hidden + hw0 + hl) * 16 + half * 8) =
           *reinterpret_cast<const bf16x8*>(&Zt[wave][hl][half * 8]);
     }
+  };
+  // A block covers a multiple of 64 rows (head grid), so tiles come in pairs.
+  if (rbeg < rend) {
+    fetch_h(rbeg, ha, la);
+    fetch_h(rbeg + 16, hb, lb);
+  }
+  for (int64_t r0 = rbeg; r0 < rend; r0 += 32) {
+    tile(r0, ha, la);
+    tile(r0 + 16, hb, lb);
   }
 
   float* out = a.partials + (static_cast<int64_t>(e) * a.blocks_per_part + blockIdx.x) * a.pstride;
