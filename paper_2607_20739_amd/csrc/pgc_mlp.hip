@@ -427,18 +427,18 @@ void mlp_head_kernel(MlpHeadArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// wgrad: dW1^T = dZ1^T X per partition, block tile 256 hidden x 112 features,
-// K = rows in steps of 64.  8 waves: wave (wh, wk) owns hidden rows
-// 64 wh .. 64 wh + 63 and the rows 32 wk .. 32 wk + 31 of every K step; the
-// two K halves are added through LDS at the end (fixed order).  Both operands
-// travel from global memory straight into LDS, two K steps ahead, through
-// three buffers (every load in the loop is such a load, so they complete in
-// order and the per-step waits count them exactly):
+// wgrad: dW1^T = dZ1^T X per partition, block tile 256 hidden x 224 features,
+// K = rows in steps of 64.  8 waves: wave (wh, wf) owns hidden rows
+// 64 wh .. 64 wh + 63 and features 112 wf .. 112 wf + 111 of the tile (a wave
+// whose features all lie past d_in skips its MFMAs).  Both operands travel
+// from global memory straight into LDS, one K step ahead, through two buffers
+// (every load in the loop is such a load, so they complete in order and the
+// per-step waits count them exactly):
 //   A (dZ1, 16-row blocked): [4 row blocks][256 hidden][2 halves of 8 rows],
 //     half s of hidden h stored at s ^ (((h >> 2) ^ (h >> 3)) & 1); the
 //     fragments are plain 16-byte reads.
-//   B (X rows): [64 rows][16 chunks of 16 bytes], the tile's 14 feature
-//     chunks plus 2 spare, chunk j of row r at slot j ^ g(r) with g(r) even
+//   B (X rows): [64 rows][32 chunks of 16 bytes], the tile's 28 feature
+//     chunks plus 4 spare, chunk j of row r at slot j ^ g(r) with g(r) even
 //     and distinct over rows {0..3, 8..11}, so that the 32-byte row pieces a
 //     transposing read gathers spread over the banks.  The fragments (8 rows
 //     of one feature per lane) come from two transposing 8-byte reads: within
@@ -446,17 +446,16 @@ void mlp_head_kernel(MlpHeadArgs a) {
 //     pieces addressed by lanes 4 j + i / 4, j = 0..3.
 // ---------------------------------------------------------------------------
 
-constexpr int kWgBM = 256, kWgBN = 112, kWgBK = 64, kWgStages = 3;
+constexpr int kWgBM = 256, kWgBN = 224, kWgBK = 64, kWgStages = 2;
 constexpr int kWgThreads = 512;
 constexpr int kWgAChunks = kWgBM * kWgBK / 8;          // 16-byte chunks of an A stage (2048)
-constexpr int kWgBRowChunks = kWgBN / 8;               // 14 per X row ...
-constexpr int kWgBRowSlots = 16;                       // ... in 16 slots
-constexpr int kWgBChunks = kWgBK * kWgBRowSlots;       // 1024
+constexpr int kWgBRowChunks = kWgBN / 8;               // 28 per X row ...
+constexpr int kWgBRowSlots = 32;                       // ... in 32 slots
+constexpr int kWgBChunks = kWgBK * kWgBRowSlots;       // 2048
 constexpr int kWgStageBytes = (kWgAChunks + kWgBChunks) * 16;
 constexpr int kWgALoads = kWgAChunks / kWgThreads, kWgBLoads = kWgBChunks / kWgThreads;
 static_assert(kWgALoads * kWgThreads == kWgAChunks && kWgBLoads * kWgThreads == kWgBChunks, "load rounds");
 static_assert(kWgStages * kWgStageBytes <= 160 * 1024, "LDS");
-static_assert(4 * 28 * 64 * 16 <= kWgStages * kWgStageBytes, "the K-half reduction fits the stages");
 
 typedef bf16 bf16x4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4v lds_bf16x4;
@@ -480,7 +479,7 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kWgStages * kWgStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int wh = wave & 3, wk = wave >> 2;
+  const int wh = wave & 3, wf = wave >> 2;
   // With at least 8 evaluated partitions, every tile of a partition goes to
   // the same XCD (workgroups are dealt to the 8 XCDs round-robin), so its L2
   // serves the dZ1 rows to all feature tiles and the X rows to all hidden
@@ -500,6 +499,7 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
   const int hb0 = (tile % htiles) * kWgBM;
   const int i0 = (tile / htiles) * kWgBN;
+  const bool active = i0 + wf * (kWgBN / 2) < a.d_in;   // uniform per wave
   const bf16* Xp = a.X + part * a.m * a.d_in;
   const bf16* dz = a.dZ1 + mlp_dz1_index(a.m_pad, a.hidden, e, 0, 0);
   const int ksteps = static_cast<int>(a.m_pad / kWgBK);
@@ -513,8 +513,8 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
     const int c = u * kWgThreads + tid, rb = c >> 9, h = (c & 511) >> 1;
     aoff[u] = (rb * a.hidden + hb0 + h) * 16 + ((c & 1) ^ wg_half_swizzle(h)) * 8;
   }
-  // B chunk c: row c / 16 at slot c % 16, holding feature chunk
-  // j = (c % 16) ^ g(row).  Spare chunks (j >= 14) and chunks past d_in read
+  // B chunk c: row c / 32 at slot c % 32, holding feature chunk
+  // j = (c % 32) ^ g(row).  Spare chunks (j >= 28) and chunks past d_in read
   // the tile's first chunk of the row; a row past the partition reads its last
   // row: all meet zeros or land in columns that are never used or stored.
   int32_t brow[kWgBLoads], bcol[kWgBLoads];
@@ -548,73 +548,61 @@ void mlp_wgrad_kernel(MlpWgradArgs a) {
   auto compute = [&](int buf) {
     const bf16* As = stage_a(buf);
     const bf16* Bs = stage_b(buf);
-    const int row = wk * 32 + lg * 8 + (lr >> 2);
-    // Feature 16 nt + 4 (lr & 3) .. + 3 sits in chunk 2 nt + ((lr & 3) >> 1), half (lr & 1).
-    auto bpos = [&](int r, int nt) {
-      return (r * kWgBRowSlots + ((2 * nt + ((lr & 3) >> 1)) ^ wg_row_swizzle(r))) * 8 + (lr & 1) * 4;
-    };
-    bf16x4v lo[7], hi[7];
 #pragma unroll
-    for (int nt = 0; nt < 7; ++nt) {
-      lo[nt] = ds_read_tr16(&Bs[bpos(row, nt)]);
-      hi[nt] = ds_read_tr16(&Bs[bpos(row + 4, nt)]);
-    }
-    const int rb = wk * 2 + (lg >> 1), half = lg & 1;
-    bf16x8 af[4];
+    for (int kk = 0; kk < 2; ++kk) {
+      const int row = kk * 32 + lg * 8 + (lr >> 2);
+      // Feature 112 wf + 16 nt + 4 (lr & 3) .. + 3 of the tile sits in chunk
+      // 14 wf + 2 nt + ((lr & 3) >> 1), half (lr & 1).
+      auto bpos = [&](int r, int nt) {
+        return (r * kWgBRowSlots + ((14 * wf + 2 * nt + ((lr & 3) >> 1)) ^ wg_row_swizzle(r))) * 8 + (lr & 1) * 4;
+      };
+      bf16x4v lo[7], hi[7];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      const int h = wh * 64 + mt * 16 + lr;
-      af[mt] = *reinterpret_cast<const bf16x8*>(&As[((rb * kWgBM + h) * 2 + (half ^ wg_half_swizzle(h))) * 8]);
-    }
-    // The transposing reads are invisible to the compiler's wait insertion:
-    // wait here, with every result tied to the wait so no use moves above it.
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(lo[4]), "+v"(lo[5]), "+v"(lo[6]),
-                   "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]), "+v"(hi[4]), "+v"(hi[5]), "+v"(hi[6]));
+      for (int nt = 0; nt < 7; ++nt) {
+        lo[nt] = ds_read_tr16(&Bs[bpos(row, nt)]);
+        hi[nt] = ds_read_tr16(&Bs[bpos(row + 4, nt)]);
+      }
+      const int rb = kk * 2 + (lg >> 1), half = lg & 1;
+      bf16x8 af[4];
 #pragma unroll
-    for (int nt = 0; nt < 7; ++nt) {
-      const bf16x8 bv = {lo[nt][0], lo[nt][1], lo[nt][2], lo[nt][3], hi[nt][0], hi[nt][1], hi[nt][2], hi[nt][3]};
+      for (int mt = 0; mt < 4; ++mt) {
+        const int h = wh * 64 + mt * 16 + lr;
+        af[mt] = *reinterpret_cast<const bf16x8*>(&As[((rb * kWgBM + h) * 2 + (half ^ wg_half_swizzle(h))) * 8]);
+      }
+      // The transposing reads are invisible to the compiler's wait insertion:
+      // wait here, with every result tied to the wait so no use moves above it.
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(lo[4]), "+v"(lo[5]), "+v"(lo[6]),
+                     "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]), "+v"(hi[4]), "+v"(hi[5]), "+v"(hi[6]));
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt], bv, acc[mt][nt]);
+      for (int nt = 0; nt < 7; ++nt) {
+        const bf16x8 bv = {lo[nt][0], lo[nt][1], lo[nt][2], lo[nt][3], hi[nt][0], hi[nt][1], hi[nt][2], hi[nt][3]};
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma_k32(af[mt], bv, acc[mt][nt]);
+      }
     }
   };
 
-  constexpr int kLoads = kWgALoads + kWgBLoads;
   issue(0, 0);
-  if (1 < ksteps) issue(1, 1);
   for (int ks = 0; ks < ksteps; ++ks) {
-    // This wave's loads of step ks have landed (step ks + 1's may still be in
-    // flight); after the barrier every wave's have, and every wave is done
-    // reading buffer (ks + 2) % 3, last used at step ks - 1.
-    if (ks + 1 < ksteps) wait_vmcnt<kLoads>();
-    else wait_vmcnt<0>();
+    // This wave's loads of step ks have landed; after the barrier every
+    // wave's have, and every wave is done reading the other buffer.
+    wait_vmcnt<0>();
     lds_barrier();
-    if (ks + 2 < ksteps) issue(ks + 2, (ks + 2) % kWgStages);
-    compute(ks % kWgStages);
+    if (ks + 1 < ksteps) issue(ks + 1, (ks + 1) % kWgStages);
+    if (active) compute(ks % kWgStages);
   }
 
-  // Add the two K halves: wk = 1 hands its sums to wk = 0 through LDS.
-  lds_barrier();
-  f32x4* red = reinterpret_cast<f32x4*>(smem) + wh * 28 * 64;
-  if (wk == 1) {
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 7; ++nt) red[(mt * 7 + nt) * 64 + lane] = acc[mt][nt];
-  }
-  __syncthreads();
-  if (wk == 1) return;
+  if (!active) return;
   float* slot = a.ring + (static_cast<int64_t>(a.plane) * a.n + part) * a.ld;
 #pragma unroll
   for (int nt = 0; nt < 7; ++nt) {
-    const int feat = i0 + nt * 16 + lr;
+    const int feat = i0 + wf * (kWgBN / 2) + nt * 16 + lr;
     if (feat >= a.d_in) continue;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      const f32x4 other = red[(mt * 7 + nt) * 64 + lane];
+    for (int mt = 0; mt < 4; ++mt)
       *reinterpret_cast<f32x4*>(slot + static_cast<int64_t>(feat) * a.hidden + hb0 + wh * 64 + mt * 16 + lg * 4) =
-          acc[mt][nt] + other;
-    }
+          acc[mt][nt];
   }
 }
 
