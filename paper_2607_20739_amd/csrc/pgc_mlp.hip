@@ -245,8 +245,10 @@ void mlp_forward_kernel(MlpForwardArgs a) {
   for (int r = tid >> 5; r < kFwBM; r += kFwThreads / 32) {
     const int64_t row = r0 + r;
     if (row < a.m)
-      *reinterpret_cast<bf16x8*>(Hp + row * a.hidden + cc * 8) =
-          *reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)]);
+      // H (2 GB per step) cannot stay in the caches until the head reads it:
+      // streaming stores keep it from evicting the reused X and W1^T tiles.
+      __builtin_nontemporal_store(*reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)]),
+                                  reinterpret_cast<bf16x8*>(Hp + row * a.hidden + cc * 8));
   }
 }
 
