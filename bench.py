@@ -10,8 +10,9 @@ over the full synthetic dataset resident in HBM.
 
 Prints one JSON line.  `value` is steps/s; `roofline` is the gradient kernel
 (the dominant one) against the 8 TB/s HBM peak, timed with HIP events around
-each of its launches inside the timed region; `cpu_baseline` is the fp64
-oracle on the host cores over a bounded sample of the same workload.
+one in every --time-every of its launches inside the timed region (an event
+pair adds ~6 us to the step it brackets); `cpu_baseline` is the fp64 oracle on
+the host cores over a bounded sample of the same workload.
 """
 
 import argparse
@@ -144,6 +145,9 @@ def main():
                     help="wall-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--all-kernel-times", action="store_true",
                     help="time every kernel with HIP events (adds event overhead to the step)")
+    ap.add_argument("--time-every", type=int, default=10,
+                    help="bracket one launch in this many of each timed kernel with HIP events "
+                         "(an event pair costs ~6 us of step time)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 20 times and exit "
                          "(a known-size reference for the HBM byte counters)")
@@ -190,6 +194,7 @@ def main():
     if args.all_kernel_times:
         timed_kernels = True
     P.pgc_set_timing(sess.ctx, timed_kernels)
+    P.pgc_set_timing_period(sess.ctx, max(1, args.time_every))
     torch.cuda.synchronize()
     start.record(stream)
     for t in range(args.warmup, total):

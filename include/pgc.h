@@ -226,6 +226,12 @@ int pgc_get_step(const pgc_ctx* ctx, int64_t* t);
 int pgc_set_timing(pgc_ctx* ctx, int kernel_mask);
 int pgc_kernel_time(pgc_ctx* ctx, int kernel, double* total_ms, int64_t* launches);
 
+/* Time only one launch in `period` of each selected kernel (the first, then
+ * every period-th; default 1 = every launch), so that the ~6 us an event pair
+ * adds to a step is paid on a sample only.  pgc_kernel_time then reports the
+ * sampled launches.  Restarts the sampling count; PGC_EINVAL if period < 1. */
+int pgc_set_timing_period(pgc_ctx* ctx, int64_t period);
+
 /* Text of a status code; last error message of a context (never NULL). */
 const char* pgc_strerror(int status);
 const char* pgc_last_error(const pgc_ctx* ctx);

@@ -59,6 +59,11 @@ class PGCSession:
                                  % (name, dtype, numel, self.device))
         _lib.pgc_step(self.ctx, X, y, w, straggler_mask, lr, self.n)
 
+    def set_stream(self, stream):
+        """Launch later steps on `stream` (a torch.cuda.Stream or a raw HIP stream handle)."""
+        handle = getattr(stream, "cuda_stream", stream)
+        _lib.pgc_set_stream(self.ctx, handle)
+
     @property
     def t(self):
         return _lib.pgc_get_step(self.ctx)

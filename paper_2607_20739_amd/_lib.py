@@ -67,6 +67,7 @@ _SIGNATURES = {
     "pgc_get_step": (ctypes.c_int, [_P, _I64P]),
     "pgc_set_timing": (ctypes.c_int, [_P, ctypes.c_int]),
     "pgc_kernel_time": (ctypes.c_int, [_P, ctypes.c_int, _F64P, _I64P]),
+    "pgc_set_timing_period": (ctypes.c_int, [_P, ctypes.c_int64]),
     "pgc_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "pgc_last_error": (ctypes.c_char_p, [_P]),
     "pgc_destroy": (ctypes.c_int, [_P]),
@@ -252,6 +253,11 @@ def pgc_set_timing(ctx, kernels):
         for k in (kernels or ()):
             mask |= 1 << int(k)
     _check(lib().pgc_set_timing(ctx, mask), ctx)
+
+
+def pgc_set_timing_period(ctx, period):
+    """Time one launch in `period` of each selected kernel."""
+    _check(lib().pgc_set_timing_period(ctx, int(period)), ctx)
 
 
 def pgc_kernel_time(ctx, kernel):

@@ -85,6 +85,8 @@ struct pgc_ctx {
   bool pipelined = true;      // false: gradient coding (every slot evaluated each step)
   std::string err;
   unsigned timing = 0;        // bit k: time kernel k
+  int64_t timing_period = 1;  // time one launch in this many of each selected kernel
+  int64_t seen[PGC_KERNEL_COUNT] = {};   // launches of each kernel since timing was set
   std::vector<Timed> pending;
   std::vector<Timed> spare;
   double total_ms[PGC_KERNEL_COUNT] = {};
@@ -183,7 +185,7 @@ int resolve_timing(pgc_ctx* ctx, bool wait) {
 template <class Fn>
 int timed_launch(pgc_ctx* ctx, int kernel, const char* what, Fn fn) {
   Timed tm;
-  const bool timed = (ctx->timing >> kernel) & 1u;
+  const bool timed = ((ctx->timing >> kernel) & 1u) && ctx->seen[kernel]++ % ctx->timing_period == 0;
   if (timed) {
     if (ctx->pending.size() >= 4096) {
       int st = resolve_timing(ctx, false);
@@ -696,6 +698,15 @@ int pgc_set_timing(pgc_ctx* ctx, int kernel_mask) {
   ctx->timing = static_cast<unsigned>(kernel_mask) & ((1u << PGC_KERNEL_COUNT) - 1u);
   std::fill(ctx->total_ms, ctx->total_ms + PGC_KERNEL_COUNT, 0.0);
   std::fill(ctx->launches, ctx->launches + PGC_KERNEL_COUNT, int64_t{0});
+  std::fill(ctx->seen, ctx->seen + PGC_KERNEL_COUNT, int64_t{0});
+  return PGC_OK;
+}
+
+int pgc_set_timing_period(pgc_ctx* ctx, int64_t period) {
+  if (ctx == nullptr) return PGC_EINVAL;
+  if (period < 1) return fail(ctx, PGC_EINVAL, "timing period must be >= 1");
+  ctx->timing_period = period;
+  std::fill(ctx->seen, ctx->seen + PGC_KERNEL_COUNT, int64_t{0});
   return PGC_OK;
 }
 
