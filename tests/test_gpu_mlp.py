@@ -63,6 +63,11 @@ SMALL = [
     # hidden = 512 (two forward column blocks, four head waves), c = n
     Workload("mlp_cr_c_eq_n", "CR", "mlp", n=3, c=3, N=3 * 160, d=120, lr=0.02, steps=7,
              policy=POLICY_UNIFORM_COUNT, cap=2, seed=33, hidden=512, classes=16),
+    # several tiles of every kernel: d_in = 456 spans three 224-wide feature tiles of the
+    # weight gradient (the last ragged), hidden = 768 three forward column tiles, m = 600
+    # three 256-row forward tiles (the last ragged)
+    Workload("mlp_cr_multi_tile", "CR", "mlp", n=4, c=2, N=4 * 600, d=456, lr=0.02, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=35, hidden=768, classes=7),
     # the real-valued code on the MLP
     Workload("mlp_real_code", "CR_REAL", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=34, hidden=256, classes=10, code_seed=3),
