@@ -255,22 +255,23 @@ void mlp_forward_kernel(MlpForwardArgs a) {
 // ---------------------------------------------------------------------------
 // head: one wave per 128 hidden columns, 16-row tiles.  The wave's partial
 // logits are summed across waves through LDS in wave order (one barrier per
-// tile).  Each wave stages its 16 x 128 tile of H and of dZ1 through its own
-// LDS area: the ReLU mask and the dW2 operand are read from there, and the
-// tile's dZ1 leaves as one contiguous 4 KiB run per wave (16-row blocked layout).
+// tile).  Each wave stages its 16 x 128 tile of H through its own LDS area,
+// from which each lane reads the four rows of one hidden unit that
+// serve as the ReLU mask and the dW2 operand.  dH comes out of the MFMA as
+// four consecutive rows of one hidden unit per lane, which is dZ1's 16-row
+// blocked layout: the tile's dZ1 leaves straight from registers, a contiguous
+// 512-byte run per store.
 // ---------------------------------------------------------------------------
 
 constexpr int kHeadCols = 128;
 constexpr int kHeadMaxWaves = kMlpMaxHidden / kHeadCols;
 constexpr int kHtLd = kHeadCols + 8;   // H tile row stride (bf16)
-constexpr int kZtLd = 16 + 8;          // dZ1 tile stride per hidden unit (bf16)
 
 __global__ __launch_bounds__(64 * kHeadMaxWaves)
 void mlp_head_kernel(MlpHeadArgs a) {
   __shared__ float zpart[2][kHeadMaxWaves][16][16];
   __shared__ float dzt[kHeadMaxWaves][16][17];
   __shared__ bf16 Ht[kHeadMaxWaves][16][kHtLd];
-  __shared__ bf16 Zt[kHeadMaxWaves][kHeadCols][kZtLd];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int waves = a.hidden / kHeadCols;
@@ -293,12 +294,11 @@ void mlp_head_kernel(MlpHeadArgs a) {
   const float b2 = lr < a.classes ? a.b2[lr] : 0.0f;
 
   f32x4 dw2[8];
-  float db1[8][4];
+  float db1[8];   // this lane's rows' share of db1[hw0 + 16 ht + lr]
 #pragma unroll
   for (int ht = 0; ht < 8; ++ht) {
     dw2[ht] = f32x4{};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) db1[ht][i] = 0.0f;
+    db1[ht] = 0.0f;
   }
   float db2 = 0.0f;
   int buf = 0;
@@ -374,27 +374,29 @@ void mlp_head_kernel(MlpHeadArgs a) {
 #pragma unroll
     for (int ht = 0; ht < 8; ++ht) {
       const int h = ht * 16;   // within the wave's columns
-      // dH^T[h + 4 lg + i][r0 + lr] = sum_c W2[h + 4 lg + i][c] dZ2[r0 + lr][c]
-      const f32x4 dh = mfma_k16(w2p[ht], dz_b, f32x4{});
-      const bf16x4 hm = *reinterpret_cast<const bf16x4*>(&Ht[wave][lr][h + lg * 4]);
+      // H[r0 + 4 lg + j][hw0 + h + lr]: the ReLU mask of dH below and the B
+      // operand of dW2.
+      bf16x4 hcol;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) hcol[j] = Ht[wave][lg * 4 + j][h + lr];
+      // dH[r0 + 4 lg + i][hw0 + h + lr] = sum_c dZ2[r0 + 4 lg + i][c] W2[hw0 + h + lr][c]
+      // (A = dZ2 rows, B = W2^T columns: the lane's four values are four
+      // consecutive rows of one hidden unit, 8 contiguous bytes of dZ1's
+      // 16-row blocked layout).
+      const f32x4 dh = mfma_k16(dz_b, w2p[ht], f32x4{});
+      bf16x4 g4;
+      float gsum = 0.0f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float g = static_cast<float>(hm[i]) > 0.0f ? dh[i] : 0.0f;
-        db1[ht][i] += g;
-        Zt[wave][h + lg * 4 + i][lr] = static_cast<bf16>(g);
+        const float g = static_cast<float>(hcol[i]) > 0.0f ? dh[i] : 0.0f;
+        gsum += g;
+        g4[i] = static_cast<bf16>(g);
       }
+      db1[ht] += gsum;
+      // The 64 lanes write one contiguous 512-byte run of the dZ1 block.
+      *reinterpret_cast<bf16x4*>(dz1 + ((r0 / 16) * hidden + hw0 + h + lr) * 16 + lg * 4) = g4;
       // dW2^T[4 lg + i][h + lr] += sum_r dZ2[r][4 lg + i] H[r][h + lr]
-      bf16x4 hb;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) hb[j] = Ht[wave][lg * 4 + j][h + lr];
-      dw2[ht] = mfma_k16(dz_a, hb, dw2[ht]);
-    }
-    // dZ1 block of rows r0 .. r0 + 15: lane writes 8 rows of hidden unit hw0 + lane/2 + 32 k.
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int hl = lane / 2 + 32 * k, half = lane & 1;
-      *reinterpret_cast<bf16x8*>(dz1 + ((r0 / 16) * hidden + hw0 + hl) * 16 + half * 8) =
-          *reinterpret_cast<const bf16x8*>(&Zt[wave][hl][half * 8]);
+      dw2[ht] = mfma_k16(dz_a, hcol, dw2[ht]);
     }
   };
   // A block covers a multiple of 64 rows (head grid), so tiles come in pairs.
@@ -412,13 +414,11 @@ void mlp_head_kernel(MlpHeadArgs a) {
   for (int ht = 0; ht < 8; ++ht) {
     const int h = hw0 + ht * 16;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      out[(lg * 4 + i) * hidden + h + lr] = dw2[ht][i];
-      float s = db1[ht][i];
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off, 64);
-      if (lr == 0) out[kMlpMaxClasses * hidden + h + lg * 4 + i] = s;
-    }
+    for (int i = 0; i < 4; ++i) out[(lg * 4 + i) * hidden + h + lr] = dw2[ht][i];
+    float s = db1[ht];
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    if (lg == 0) out[kMlpMaxClasses * hidden + h + lr] = s;
   }
   if (wave == 0) {
     float s = db2;
