@@ -265,7 +265,12 @@ void mlp_forward_kernel(MlpForwardArgs a) {
 
 constexpr int kHeadCols = 128;
 constexpr int kHeadMaxWaves = kMlpMaxHidden / kHeadCols;
-constexpr int kHtLd = kHeadCols + 8;   // H tile row stride (bf16)
+constexpr int kHtLd = kHeadCols + 16;  // H tile row stride (bf16): 288 bytes, so the four
+                                       // 32-byte row pieces of a transposing read hit
+                                       // distinct banks
+
+typedef bf16 bf16x4t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4t lds_bf16x4t;
 
 __global__ __launch_bounds__(64 * kHeadMaxWaves)
 void mlp_head_kernel(MlpHeadArgs a) {
@@ -376,9 +381,12 @@ void mlp_head_kernel(MlpHeadArgs a) {
       const int h = ht * 16;   // within the wave's columns
       // H[r0 + 4 lg + j][hw0 + h + lr]: the ReLU mask of dH below and the B
       // operand of dW2.
-      bf16x4 hcol;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) hcol[j] = Ht[wave][lg * 4 + j][h + lr];
+      // One transposing read: within each 16-lane group, lane i receives
+      // element i % 4 of the 4-element row pieces addressed by lanes 4 j + i / 4,
+      // so lane q addresses row 4 lg + q / 4, columns h + 4 (q % 4) .. + 3.
+      const bf16x4t ht4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+          (lds_bf16x4t*)&Ht[wave][lg * 4 + (lr >> 2)][h + 4 * (lr & 3)]);
+      const bf16x4 hcol = {ht4[0], ht4[1], ht4[2], ht4[3]};
       // dH[r0 + 4 lg + i][hw0 + h + lr] = sum_c dZ2[r0 + 4 lg + i][c] W2[hw0 + h + lr][c]
       // (A = dZ2 rows, B = W2^T columns: the lane's four values are four
       // consecutive rows of one hidden unit, 8 contiguous bytes of dZ1's
