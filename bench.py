@@ -110,10 +110,14 @@ def cpu_baseline(w, X, y, beta0, budget_s):
               keep_coded=False, keep_alpha=False)
         return time.perf_counter() - t0
 
-    # Size the sample from a 6-step probe (whose time includes the one-time
-    # setup, so the estimate errs on the short side).
-    per_step = max(run(6) / 6, 1e-6)
-    steps = int(max(2, min(max_steps, budget_s / per_step)))
+    # Size the sample from two probes: their difference is the marginal cost
+    # of a step, the rest the one-time setup (the oracle's fp64 copy of X).
+    # The estimate is floored at a quarter of the longer probe's average, so a
+    # noisy difference cannot inflate the sample.
+    t6, t12 = run(6), run(12)
+    per_step = max((t12 - t6) / 6, t12 / 12 / 4, 1e-6)
+    setup = max(t6 - 6 * per_step, 0.0)
+    steps = int(max(2, min(max_steps, (budget_s - setup) / per_step)))
     elapsed = run(steps)
     threads = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
     cores = min(max(threads) if threads else 1, len(os.sched_getaffinity(0)))
