@@ -110,14 +110,16 @@ def cpu_baseline(w, X, y, beta0, budget_s):
               keep_coded=False, keep_alpha=False)
         return time.perf_counter() - t0
 
-    # Size the sample from two probes: their difference is the marginal cost
-    # of a step, the rest the one-time setup (the oracle's fp64 copy of X).
+    # Size the sample from two probes (10 and 30 steps): their difference is
+    # the marginal cost of a step, the rest the one-time setup (the oracle's
+    # fp64 copy of X).
     # The estimate is floored at a quarter of the longer probe's average, so a
     # noisy difference cannot inflate the sample.
-    t6, t12 = run(6), run(12)
-    per_step = max((t12 - t6) / 6, t12 / 12 / 4, 1e-6)
-    setup = max(t6 - 6 * per_step, 0.0)
+    t_short, t_long = run(10), run(30)
+    per_step = max((t_long - t_short) / 20, t_long / 30 / 4, 1e-6)
+    setup = max(t_short - 10 * per_step, 0.0)
     steps = int(max(2, min(max_steps, (budget_s - setup) / per_step)))
+    log("oracle: ~%.1f ms per step, ~%.1f s setup; timing %d steps" % (per_step * 1e3, setup, steps))
     elapsed = run(steps)
     threads = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
     cores = min(max(threads) if threads else 1, len(os.sched_getaffinity(0)))
@@ -145,7 +147,7 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--all-kernel-times", action="store_true",
                     help="time every kernel with HIP events (adds event overhead to the step)")
