@@ -73,8 +73,17 @@ void reduce_code_kernel(ReduceCodeArgs a) {
     const int64_t col = col0 + pair % kFusedCols;
     if (col >= ca.q) continue;
     const float* p = a.partials + static_cast<int64_t>(e) * a.blocks_per_part * ca.q + col;
+    // Loads go out 32 at a time (one memory latency per 32 partials); the
+    // fp64 sum still runs in block order.
     double s = 0.0;
     int b = 0;
+    for (; b + 32 <= a.blocks_per_part; b += 32) {
+      float t[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) t[i] = p[static_cast<int64_t>(b + i) * ca.q];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) s += static_cast<double>(t[i]);
+    }
     for (; b + 8 <= a.blocks_per_part; b += 8) {
       float t[8];
 #pragma unroll
