@@ -40,6 +40,29 @@ __device__ __forceinline__ f32x4 mfma_k16(bf16x4 a, bf16x4 b, f32x4 c) {
 template <class T>
 __device__ __forceinline__ T load_vec(const bf16* p) { return *reinterpret_cast<const T*>(p); }
 
+// Reductions over each 16-lane row of the wave with DPP lane moves (register
+// to register, no LDS round trip): swap neighbours, swap pairs, mirror each
+// half row, mirror the row.  After the two quad steps each lane holds its
+// quad's result; each mirror step combines a lane with one holding the other
+// half's result, so every lane of the row ends with the same value.
+template <int ctrl>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xF, 0xF, true));
+}
+constexpr int kDppSwap1 = 0xB1, kDppSwap2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_move<kDppSwap1>(v));
+  v = fmaxf(v, dpp_move<kDppSwap2>(v));
+  v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
+  return fmaxf(v, dpp_move<kDppMirror>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_move<kDppSwap1>(v);
+  v += dpp_move<kDppSwap2>(v);
+  v += dpp_move<kDppHalfMirror>(v);
+  return v + dpp_move<kDppMirror>(v);
+}
+
 // ---------------------------------------------------------------------------
 // cast
 // ---------------------------------------------------------------------------
@@ -355,13 +378,9 @@ void mlp_head_kernel(MlpHeadArgs a) {
       const int64_t row = r0 + lg * 4 + i;
       const bool live = lr < a.classes;
       const float v = live ? s + b2 : -INFINITY;
-      float mx = v;
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      const float mx = row16_max(v);
       const float ex = live ? expf(v - mx) : 0.0f;
-      float sum = ex;
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+      const float sum = row16_sum(ex);
       dz2[i] = (row < a.m && live) ? (ex / sum - (lr == label[i] ? 1.0f : 0.0f)) * a.inv_m : 0.0f;
       db2 += dz2[i];
     }
