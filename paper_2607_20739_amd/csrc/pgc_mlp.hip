@@ -21,6 +21,7 @@
 #include <cmath>
 
 #include "pgc_kernels.h"
+#include "pgc_lanes.h"
 
 namespace pgc {
 namespace {
@@ -39,29 +40,6 @@ __device__ __forceinline__ f32x4 mfma_k16(bf16x4 a, bf16x4 b, f32x4 c) {
 
 template <class T>
 __device__ __forceinline__ T load_vec(const bf16* p) { return *reinterpret_cast<const T*>(p); }
-
-// Reductions over each 16-lane row of the wave with DPP lane moves (register
-// to register, no LDS round trip): swap neighbours, swap pairs, mirror each
-// half row, mirror the row.  After the two quad steps each lane holds its
-// quad's result; each mirror step combines a lane with one holding the other
-// half's result, so every lane of the row ends with the same value.
-template <int ctrl>
-__device__ __forceinline__ float dpp_move(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xF, 0xF, true));
-}
-constexpr int kDppSwap1 = 0xB1, kDppSwap2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
-__device__ __forceinline__ float row16_max(float v) {
-  v = fmaxf(v, dpp_move<kDppSwap1>(v));
-  v = fmaxf(v, dpp_move<kDppSwap2>(v));
-  v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
-  return fmaxf(v, dpp_move<kDppMirror>(v));
-}
-__device__ __forceinline__ float row16_sum(float v) {
-  v += dpp_move<kDppSwap1>(v);
-  v += dpp_move<kDppSwap2>(v);
-  v += dpp_move<kDppHalfMirror>(v);
-  return v + dpp_move<kDppMirror>(v);
-}
 
 // ---------------------------------------------------------------------------
 // cast
