@@ -146,6 +146,7 @@ int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes);
  *        their coded gradients are left out of the decode (Sec. V-B).
  * t = 0 is the warm-up: every worker evaluates all c held partitions at w
  * (Sec. IV-A).  For t >= 1 worker i evaluates its slot (t - 1) mod c.
+ * lr must be finite (PGC_EINVAL otherwise).
  * Errors (PGC_EINVAL, PGC_ESTRAGGLERS, PGC_ESINGULAR, PGC_ESTATE) are detected
  * before any work is enqueued: a rejected step has no effect and t does not
  * advance.  Returns without synchronising the stream. */

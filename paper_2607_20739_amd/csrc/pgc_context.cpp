@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <cmath>
 #include <string>
 #include <vector>
 
@@ -622,6 +623,7 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
   if (!ctx->configured) return fail(ctx, PGC_ESTATE, "pgc_configure first");
   if (ctx->ws == nullptr) return fail(ctx, PGC_ESTATE, "pgc_bind_workspace first");
   if (!X || !y || !w || !straggler_mask) return fail(ctx, PGC_EINVAL, "null pointer");
+  if (!std::isfinite(lr)) return fail(ctx, PGC_EINVAL, "learning rate must be finite");
   pgc::Decode dec;
   std::string err;
   switch (pgc::decode_coefficients(ctx->scheme, ctx->n, ctx->c, ctx->B, straggler_mask, &dec, &err)) {

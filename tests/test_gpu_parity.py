@@ -198,6 +198,10 @@ def test_rejected_step_has_no_effect():
         with pytest.raises(P.PGCError) as e:
             sess.step(X, y, wv, np.array([1, 1, 0, 0], np.uint8), w.lr)   # a whole FR group straggles
         assert e.value.status == P.PGC_ESTRAGGLERS
+        for bad_lr in (float("nan"), float("inf"), -float("inf")):
+            with pytest.raises(P.PGCError) as e:
+                sess.step(X, y, wv, np.zeros(4, np.uint8), bad_lr)
+            assert e.value.status == P.PGC_EINVAL
         torch.cuda.synchronize()
         assert sess.t == 1
         assert torch.equal(wv, before)
