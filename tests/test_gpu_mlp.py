@@ -68,6 +68,10 @@ SMALL = [
     # three 256-row forward tiles (the last ragged)
     Workload("mlp_cr_multi_tile", "CR", "mlp", n=4, c=2, N=4 * 600, d=456, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=35, hidden=768, classes=7),
+    # five rows per partition: one ragged 16-row head tile, one 64-row weight-gradient K step,
+    # and a forward tile that is almost all clamped rows
+    Workload("mlp_cr_tiny_partitions", "CR", "mlp", n=4, c=2, N=4 * 5, d=16, lr=0.05, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=36, hidden=256, classes=4),
     # the real-valued code on the MLP
     Workload("mlp_real_code", "CR_REAL", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=34, hidden=256, classes=10, code_seed=3),

@@ -107,6 +107,11 @@ EDGE = [
              policy=POLICY_EXACT, cap=0, seed=19),
     Workload("edge_fr_logistic_d8191", "FR", "logistic", n=4, c=4, N=4 * 37, d=8191, lr=0.05, steps=6,
              policy=POLICY_UNIFORM_COUNT, cap=3, seed=20),
+    # degenerate partitions: one row each, and two rows each with a masked float4 column tail
+    Workload("edge_cr_logistic_m1", "CR", "logistic", n=8, c=3, N=8, d=64, lr=0.3, steps=7,
+             policy=POLICY_UNIFORM_COUNT, cap=2, seed=23),
+    Workload("edge_fr_lsq_m2", "FR", "lsq", n=6, c=2, N=12, d=100, lr=0.05, steps=6,
+             policy=POLICY_EXACT, cap=1, seed=24),
     # every worker may straggle up to s = 7 in one step
     Workload("edge_cr_logistic_heavy", "CR", "logistic", n=16, c=8, N=16 * 64, d=512, lr=0.1, steps=12,
              policy=POLICY_BERNOULLI, cap=7, p=0.4, seed=21),
