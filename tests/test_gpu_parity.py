@@ -112,6 +112,11 @@ EDGE = [
              policy=POLICY_UNIFORM_COUNT, cap=2, seed=23),
     Workload("edge_fr_lsq_m2", "FR", "lsq", n=6, c=2, N=12, d=100, lr=0.05, steps=6,
              policy=POLICY_EXACT, cap=1, seed=24),
+    # the largest worker count: 256 decode weights and coded words per step
+    Workload("edge_cr_logistic_n256", "CR", "logistic", n=256, c=4, N=256 * 8, d=64, lr=0.2, steps=7,
+             policy=POLICY_BERNOULLI, cap=3, p=0.01, seed=25),
+    Workload("edge_fr_lsq_n256_c8", "FR", "lsq", n=256, c=8, N=256 * 4, d=32, lr=0.05, steps=10,
+             policy=POLICY_UNIFORM_COUNT, cap=7, seed=26),
     # every worker may straggle up to s = 7 in one step
     Workload("edge_cr_logistic_heavy", "CR", "logistic", n=16, c=8, N=16 * 64, d=512, lr=0.1, steps=12,
              policy=POLICY_BERNOULLI, cap=7, p=0.4, seed=21),
