@@ -221,6 +221,18 @@ def main():
         print("non-finite weights after the timed steps", file=sys.stderr)
         return 1
 
+    # The warm-up step t = 0 (every worker evaluates all of its partitions),
+    # timed on its own after starting the session over.
+    sess.restart()
+    w_fill = beta0.clone()
+    torch.cuda.synchronize()
+    start.record(stream)
+    sess.step(X, y, w_fill, masks[0], w.lr)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    warmup_step_ms = start.elapsed_time(stop)
+    del w_fill
+
     ms_per_step = elapsed_ms / args.steps
     steps_per_s = 1000.0 / ms_per_step
     grad_bytes, step_bytes = algorithmic_bytes(w)
@@ -262,6 +274,7 @@ def main():
         "samples_per_s": {"unique_rows": rows * steps_per_s, "worker_samples": w.N * steps_per_s},
         "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
         "kernel_ms_per_launch": per_launch,
+        "warmup_step_ms": warmup_step_ms,
         "roofline": roofline,
         "cpu_baseline": baseline,
     }

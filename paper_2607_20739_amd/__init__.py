@@ -59,6 +59,11 @@ class PGCSession:
                                  % (name, dtype, numel, self.device))
         _lib.pgc_step(self.ctx, X, y, w, straggler_mask, lr, self.n)
 
+    def restart(self):
+        """Start over at t = 0 (the warm-up step) by binding the workspace again;
+        the next step refills the whole ring."""
+        _lib.pgc_bind_workspace(self.ctx, self.workspace, _lib.pgc_workspace_bytes(self.ctx))
+
     def set_stream(self, stream):
         """Launch later steps on `stream` (a torch.cuda.Stream or a raw HIP stream handle)."""
         handle = getattr(stream, "cuda_stream", stream)

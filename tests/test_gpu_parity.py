@@ -196,6 +196,30 @@ def test_runs_are_bitwise_reproducible():
     assert torch.equal(w1, w2)
 
 
+def test_restart_reproduces_the_run():
+    """Binding the workspace again starts over at t = 0: the same steps then
+    give bitwise the same weights, ring and decoded gradient."""
+    w = WORKLOADS["crreal_lsq_n8_c3_d1024"].resized(N=8 * 2048, steps=5)
+    _announce("restart")
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    sess = gpu_session(w)
+    try:
+        runs = []
+        for _ in range(2):
+            wv = beta0.clone()
+            for t in range(w.steps):
+                sess.step(X, y, wv, masks[t], w.lr)
+            runs.append((wv, sess.decoded(), sess.ring(3, 1), sess.t))
+            sess.restart()
+            assert sess.t == 0
+        (w1, g1, r1, t1), (w2, g2, r2, t2) = runs
+        assert t1 == t2 == w.steps
+        assert torch.equal(w1, w2) and torch.equal(g1, g2) and torch.equal(r1, r2)
+    finally:
+        sess.close()
+
+
 def test_rejected_step_has_no_effect():
     w = WORKLOADS["fr_logistic_n4_c2_d64"]
     _announce("rejected step")
