@@ -222,16 +222,25 @@ def main():
         return 1
 
     # The warm-up step t = 0 (every worker evaluates all of its partitions),
-    # timed on its own after starting the session over.
+    # timed on its own after starting the session over.  The same session
+    # then repeats every step untimed, reading the decoded gradient out after
+    # each one; its final weights must equal the timed pass's bit for bit.
     sess.restart()
-    w_fill = beta0.clone()
+    w_check = beta0.clone()
     torch.cuda.synchronize()
     start.record(stream)
-    sess.step(X, y, w_fill, masks[0], w.lr)
+    sess.step(X, y, w_check, masks[0], w.lr)
     stop.record(stream)
     torch.cuda.synchronize()
     warmup_step_ms = start.elapsed_time(stop)
-    del w_fill
+    for t in range(1, total):
+        sess.step(X, y, w_check, masks[t], w.lr)
+        sess.decoded()
+    torch.cuda.synchronize()
+    reproduced = bool(torch.equal(w_check, wv))
+    if not reproduced:
+        log("the repeated pass did not reproduce the timed pass's weights bit for bit")
+    del w_check
 
     ms_per_step = elapsed_ms / args.steps
     steps_per_s = 1000.0 / ms_per_step
@@ -275,6 +284,7 @@ def main():
         "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
         "kernel_ms_per_launch": per_launch,
         "warmup_step_ms": warmup_step_ms,
+        "timed_pass_reproduced": reproduced,
         "roofline": roofline,
         "cpu_baseline": baseline,
     }
