@@ -216,6 +216,31 @@ int pgc_read_ring(const pgc_ctx* ctx, int worker, int slot, float* dev_out);
 int pgc_read_coded(const pgc_ctx* ctx, int index, float* dev_out);
 int pgc_read_decoded(const pgc_ctx* ctx, float* dev_out);
 
+/* Checkpoint and resume of the pipeline.  A pipelined step reads the latest
+ * gradient of every partition a worker holds, most of them computed at
+ * earlier steps (Sec. IV-A, Sec. VI-A), so a run resumes on the same
+ * trajectory only if those copies come back; starting over would repeat the
+ * warm-up (Sec. IV-A) at the current w and change every later step.  The saved
+ * state is the step counter t and the gradient ring.  The parameter vector w
+ * is the caller's own and is checkpointed by the caller.
+ *
+ * pgc_state_bytes: bytes of a saved state for this configured context (a
+ *   256-byte header, then c planes of n gradient copies for CR and CR_REAL,
+ *   one for FR and IS_SGD).  Host only.
+ * pgc_save_state: writes the state into caller-owned device memory
+ *   (`bytes` >= pgc_state_bytes, 16-byte aligned) on the context stream,
+ *   asynchronously, as of the work enqueued before the call.  Needs a bound
+ *   workspace.
+ * pgc_load_state: restores a state saved by a context of the same scheme, n,
+ *   c, model shape and (CR_REAL) code seed: the ring, and t.  Synchronises the
+ *   context stream to read and check the header first; a buffer that is not a
+ *   saved state, or one from another configuration, is rejected with
+ *   PGC_EINVAL before anything changes.  Pipelining on or off is not part of
+ *   the state. */
+int pgc_state_bytes(const pgc_ctx* ctx, size_t* bytes);
+int pgc_save_state(const pgc_ctx* ctx, void* dev_out, size_t bytes);
+int pgc_load_state(pgc_ctx* ctx, const void* dev_in, size_t bytes);
+
 /* Current step counter t (the number of completed pgc_step calls since configure/bind). */
 int pgc_get_step(const pgc_ctx* ctx, int64_t* t);
 

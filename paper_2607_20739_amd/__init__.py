@@ -64,6 +64,18 @@ class PGCSession:
         the next step refills the whole ring."""
         _lib.pgc_bind_workspace(self.ctx, self.workspace, _lib.pgc_workspace_bytes(self.ctx))
 
+    def save_state(self):
+        """The pipeline state (step counter and gradient ring) in a new uint8 GPU
+        tensor, filled on the session's stream."""
+        import torch
+        out = torch.empty(_lib.pgc_state_bytes(self.ctx), dtype=torch.uint8, device=self.device)
+        _lib.pgc_save_state(self.ctx, out)
+        return out
+
+    def load_state(self, state):
+        """Resume from a state saved by a session of the same configuration."""
+        _lib.pgc_load_state(self.ctx, state)
+
     def set_stream(self, stream):
         """Launch later steps on `stream` (a torch.cuda.Stream or a raw HIP stream handle)."""
         handle = getattr(stream, "cuda_stream", stream)

@@ -64,6 +64,9 @@ _SIGNATURES = {
     "pgc_read_ring": (ctypes.c_int, [_P, ctypes.c_int, ctypes.c_int, _P]),
     "pgc_read_coded": (ctypes.c_int, [_P, ctypes.c_int, _P]),
     "pgc_read_decoded": (ctypes.c_int, [_P, _P]),
+    "pgc_state_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
+    "pgc_save_state": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
+    "pgc_load_state": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
     "pgc_get_step": (ctypes.c_int, [_P, _I64P]),
     "pgc_set_timing": (ctypes.c_int, [_P, ctypes.c_int]),
     "pgc_kernel_time": (ctypes.c_int, [_P, ctypes.c_int, _F64P, _I64P]),
@@ -223,6 +226,24 @@ def pgc_splitmix64(seed, index):
     out = ctypes.c_uint64()
     _check(lib().pgc_splitmix64(int(seed), int(index), ctypes.byref(out)))
     return out.value
+
+
+def pgc_state_bytes(ctx):
+    out = ctypes.c_size_t()
+    _check(lib().pgc_state_bytes(ctx, ctypes.byref(out)), ctx)
+    return out.value
+
+
+def pgc_save_state(ctx, out, nbytes=None):
+    if nbytes is None:
+        nbytes = out.numel() * out.element_size()
+    _check(lib().pgc_save_state(ctx, _P(_dev(out)), int(nbytes)), ctx)
+
+
+def pgc_load_state(ctx, state, nbytes=None):
+    if nbytes is None:
+        nbytes = state.numel() * state.element_size()
+    _check(lib().pgc_load_state(ctx, _P(_dev(state)), int(nbytes)), ctx)
 
 
 def pgc_read_ring(ctx, worker, slot, out):

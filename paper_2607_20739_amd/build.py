@@ -22,7 +22,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpgc.so")
-SOURCES = ["pgc_codes.cpp", "pgc_context.cpp", "pgc_linear.hip", "pgc_code.hip", "pgc_mlp.hip"]
+SOURCES = sorted(f for f in os.listdir(CSRC) if f.endswith((".cpp", ".hip")))
 ARCH = "gfx950"
 
 

@@ -664,6 +664,86 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
   return PGC_OK;
 }
 
+namespace {
+
+size_t ring_bytes(const pgc_ctx* ctx) {
+  return sizeof(float) * static_cast<size_t>(ctx->planes) * ctx->n * ctx->ld;
+}
+
+pgc::StateHeader state_header(const pgc_ctx* ctx) {
+  pgc::StateHeader h{};
+  h.magic = pgc::kStateMagic;
+  h.version = pgc::kStateVersion;
+  h.t = ctx->t;
+  h.N = ctx->cfg.N;
+  h.q = ctx->d;
+  h.ld = ctx->ld;
+  h.code_seed = ctx->scheme == PGC_CR_REAL ? ctx->cfg.code_seed : 0;
+  h.scheme = ctx->scheme;
+  h.n = ctx->n;
+  h.c = ctx->c;
+  h.model = ctx->cfg.model;
+  h.d_in = ctx->cfg.d_in;
+  h.hidden = ctx->cfg.hidden;
+  h.classes = ctx->cfg.classes;
+  h.planes = ctx->planes;
+  return h;
+}
+
+// Checks shared by save and load; the state holds the ring, so a workspace
+// must be bound.
+int state_args(const pgc_ctx* ctx, const void* dev, size_t bytes) {
+  if (ctx == nullptr) return PGC_EINVAL;
+  if (!ctx->configured) return fail(ctx, PGC_ESTATE, "pgc_configure first");
+  if (ctx->ws == nullptr) return fail(ctx, PGC_ESTATE, "pgc_bind_workspace first");
+  if (dev == nullptr) return fail(ctx, PGC_EINVAL, "null state buffer");
+  if (reinterpret_cast<uintptr_t>(dev) % 16 != 0) return fail(ctx, PGC_EINVAL, "state buffer must be 16-byte aligned");
+  const size_t need = pgc::kStateHeaderBytes + ring_bytes(ctx);
+  if (bytes < need) return fail(ctx, PGC_EINVAL, "state buffer too small: need " + std::to_string(need) + " bytes");
+  return PGC_OK;
+}
+
+}  // namespace
+
+int pgc_state_bytes(const pgc_ctx* ctx, size_t* bytes) {
+  if (ctx == nullptr || bytes == nullptr) return PGC_EINVAL;
+  if (!ctx->configured) return fail(ctx, PGC_ESTATE, "pgc_configure first");
+  *bytes = pgc::kStateHeaderBytes + ring_bytes(ctx);
+  return PGC_OK;
+}
+
+int pgc_save_state(const pgc_ctx* ctx, void* dev_out, size_t bytes) {
+  const int st = state_args(ctx, dev_out, bytes);
+  if (st != PGC_OK) return st;
+  pgc_ctx* mctx = const_cast<pgc_ctx*>(ctx);
+  hipError_t e = pgc::launch_write_state_header(state_header(ctx), dev_out, ctx->stream);
+  if (e != hipSuccess) return device_fail(mctx, e, "writing the state header");
+  e = hipMemcpyAsync(static_cast<char*>(dev_out) + pgc::kStateHeaderBytes, ctx->ws + ctx->off_ring, ring_bytes(ctx),
+                     hipMemcpyDeviceToDevice, ctx->stream);
+  return e == hipSuccess ? PGC_OK : device_fail(mctx, e, "copying the ring");
+}
+
+int pgc_load_state(pgc_ctx* ctx, const void* dev_in, size_t bytes) {
+  const int st = state_args(ctx, dev_in, bytes);
+  if (st != PGC_OK) return st;
+  pgc::StateHeader h{};
+  hipError_t e = hipMemcpyAsync(&h, dev_in, sizeof(h), hipMemcpyDeviceToHost, ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return device_fail(ctx, e, "reading the state header");
+  if (h.magic != pgc::kStateMagic || h.version != pgc::kStateVersion)
+    return fail(ctx, PGC_EINVAL, "not a saved PGC state (magic or version)");
+  pgc::StateHeader mine = state_header(ctx);
+  mine.t = h.t;
+  if (std::memcmp(&h, &mine, sizeof(h)) != 0)
+    return fail(ctx, PGC_EINVAL, "saved state belongs to a different scheme, code or shape");
+  if (h.t < 0) return fail(ctx, PGC_EINVAL, "saved state has a negative step counter");
+  e = hipMemcpyAsync(ctx->ws + ctx->off_ring, static_cast<const char*>(dev_in) + pgc::kStateHeaderBytes,
+                     ring_bytes(ctx), hipMemcpyDeviceToDevice, ctx->stream);
+  if (e != hipSuccess) return device_fail(ctx, e, "restoring the ring");
+  ctx->t = h.t;
+  return PGC_OK;
+}
+
 int pgc_read_ring(const pgc_ctx* ctx, int worker, int slot, float* dev_out) {
   if (ctx == nullptr || dev_out == nullptr) return PGC_EINVAL;
   if (ctx->ws == nullptr) return fail(ctx, PGC_ESTATE, "no workspace bound");

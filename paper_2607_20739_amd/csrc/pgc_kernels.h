@@ -167,4 +167,21 @@ struct MlpReduceArgs {
 };
 hipError_t launch_mlp_reduce(const MlpReduceArgs& a, hipStream_t s);
 
+// Header of a saved pipeline state: the first kStateHeaderBytes bytes of the
+// caller's buffer (the rest of the struct's space is zero), followed by the
+// ring.  Every field but t must match the loading context.
+struct StateHeader {
+  uint64_t magic;     // kStateMagic
+  uint64_t version;   // kStateVersion
+  int64_t t, N, q, ld;
+  uint64_t code_seed;
+  int32_t scheme, n, c, model, d_in, hidden, classes, planes;
+};
+constexpr uint64_t kStateMagic = 0x4554415453434750ull;   // the bytes "PGCSTATE"
+constexpr uint64_t kStateVersion = 1;
+constexpr size_t kStateHeaderBytes = 256;
+static_assert(sizeof(StateHeader) <= kStateHeaderBytes && sizeof(StateHeader) % 8 == 0, "state header");
+// Writes h (zero-padded to kStateHeaderBytes) to out, which is 8-byte aligned.
+hipError_t launch_write_state_header(const StateHeader& h, void* out, hipStream_t s);
+
 }  // namespace pgc

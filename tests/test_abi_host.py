@@ -205,3 +205,29 @@ def test_workspace_size_covers_ring_coded_and_partials():
             assert P.pgc_workspace_bytes(ctx) % 256 == 0
         finally:
             P.pgc_destroy(ctx)
+
+
+def test_state_size_is_the_header_and_the_ring():
+    """A saved state holds a 256-byte header and every ring slot (c planes for
+    CR, one for FR), slots padded to a multiple of 256 floats."""
+    for scheme, n, c, d, model in [("FR", 4, 2, 64, "logistic"), ("CR_REAL", 8, 3, 1000, "lsq"),
+                                   ("CR", 16, 4, 300, "logistic"), ("IS_SGD", 5, 1, 8, "lsq")]:
+        ctx = _ctx(scheme, n, c, d=d, N=n * 8, model=model)
+        try:
+            planes = 1 if scheme in ("FR", "IS_SGD") else c
+            ld = -(-d // 256) * 256
+            assert P.pgc_state_bytes(ctx) == 256 + 4 * planes * n * ld
+            # Saving and loading need the ring, i.e. a bound workspace.
+            for call in (P.pgc_save_state, P.pgc_load_state):
+                with pytest.raises(P.PGCError) as e:
+                    call(ctx, 1 << 20, 1 << 30)
+                assert e.value.status == P.PGC_ESTATE
+        finally:
+            P.pgc_destroy(ctx)
+    ctx = P.pgc_init("CR", 8, 3, 16)
+    try:
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_state_bytes(ctx)                     # not configured
+        assert e.value.status == P.PGC_ESTATE
+    finally:
+        P.pgc_destroy(ctx)

@@ -101,6 +101,30 @@ def test_mlp_runs_are_bitwise_reproducible():
     assert torch.equal(w1, w2)
 
 
+def test_mlp_resume_from_saved_state_is_bitwise_identical():
+    w = SMALL[0]
+    _announce("mlp resume")
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    k = 3
+    a, b = gpu_session(w), gpu_session(w)
+    try:
+        wa = beta0.clone()
+        for t in range(k):
+            a.step(X, y, wa, masks[t], w.lr)
+        state = a.save_state()
+        wb = wa.clone()
+        for t in range(k, w.steps):
+            a.step(X, y, wa, masks[t], w.lr)
+        b.load_state(state)
+        for t in range(k, w.steps):
+            b.step(X, y, wb, masks[t], w.lr)
+        assert torch.equal(wa, wb)
+    finally:
+        a.close()
+        b.close()
+
+
 def test_full_size_mlp_ring_holds_partition_gradients():
     """Full size (N = 1048576), lr = 0: sampled partitions' ring copies equal the
     oracle's gradient at beta0, computed one partition at a time."""

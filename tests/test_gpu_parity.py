@@ -220,6 +220,77 @@ def test_restart_reproduces_the_run():
         sess.close()
 
 
+RESUME = [
+    WORKLOADS["fr_logistic_n4_c2_d64"],
+    WORKLOADS["crreal_lsq_n8_c3_d1024"].resized(N=8 * 2048, steps=9),
+    Workload("resume_cr_logistic", "CR", "logistic", n=6, c=3, N=6 * 500, d=512, lr=0.1, steps=10,
+             policy=POLICY_UNIFORM_COUNT, cap=2, seed=27),
+]
+
+
+@pytest.mark.parametrize("k", [0, 1, 4])
+@pytest.mark.parametrize("w", RESUME, ids=[w.name for w in RESUME])
+def test_resume_from_saved_state_is_bitwise_identical(w, k):
+    """Run T steps straight, or k steps, save, and finish in a new session that
+    loads the state: the weights and the last decoded gradient agree bit for
+    bit.  Starting a new session without the state (a fresh warm-up at the
+    checkpoint's w) lands elsewhere once the ring holds older copies."""
+    _announce("%s resume after %d steps" % (w.name, k))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    a, b, fresh = gpu_session(w), gpu_session(w), gpu_session(w)
+    try:
+        wa = beta0.clone()
+        for t in range(k):
+            a.step(X, y, wa, masks[t], w.lr)
+        state = a.save_state()
+        w_saved = wa.clone()
+        for t in range(k, w.steps):
+            a.step(X, y, wa, masks[t], w.lr)
+        b.load_state(state)
+        assert b.t == k
+        wb = w_saved.clone()
+        for t in range(k, w.steps):
+            b.step(X, y, wb, masks[t], w.lr)
+        assert torch.equal(wa, wb)
+        assert torch.equal(a.decoded(), b.decoded())
+        if k >= 2:
+            wf = w_saved.clone()
+            for t in range(k, w.steps):
+                fresh.step(X, y, wf, masks[t], w.lr)
+            assert not torch.equal(wf, wa)
+    finally:
+        for sess in (a, b, fresh):
+            sess.close()
+
+
+def test_load_state_rejects_foreign_or_broken_buffers():
+    w = WORKLOADS["crreal_lsq_n8_c3_d1024"].resized(N=8 * 512, steps=4)
+    other = Workload("same_size_cr", "CR", "lsq", n=8, c=3, N=8 * 512, d=1024, lr=0.01, steps=4,
+                     policy=POLICY_EXACT, cap=1, seed=2)
+    _announce("state rejection")
+    X, y, beta0 = make_inputs(w, device="cuda")
+    a, b = gpu_session(w), gpu_session(other)
+    try:
+        wv = beta0.clone()
+        for t, mask in enumerate(gpu_masks(w)):
+            a.step(X, y, wv, mask, w.lr)
+        state = a.save_state()
+        assert P.pgc_state_bytes(b.ctx) == state.numel()   # same size, another scheme
+        bad = [(b, state), (a, torch.zeros_like(state)), (a, state[:-256]), (a, state[1:])]
+        for sess, buf in bad:
+            t_before = sess.t
+            with pytest.raises(P.PGCError) as e:
+                sess.load_state(buf)
+            assert e.value.status == P.PGC_EINVAL
+            assert sess.t == t_before
+        a.load_state(state)
+        assert a.t == w.steps
+    finally:
+        a.close()
+        b.close()
+
+
 def test_rejected_step_has_no_effect():
     w = WORKLOADS["fr_logistic_n4_c2_d64"]
     _announce("rejected step")
