@@ -174,6 +174,60 @@ def test_baseline_trajectory_matches_oracle(w, pipelined):
     _check_trajectory(w, X, y, beta0, pipelined=pipelined)
 
 
+# Hand-made straggler patterns (each admissible: at most s = c - 1 stragglers,
+# and an FR group never loses all of its members).
+ADVERSARIAL = [
+    # FR: group 0 keeps c - 1 stragglers at every step
+    (Workload("adv_fr_group_short", "FR", "logistic", n=6, c=3, N=6 * 300, d=256, lr=0.2, steps=9,
+              policy=POLICY_EXACT, cap=0, seed=28),
+     lambda t, n: [1 if i in (0, 1) else 0 for i in range(n)]),
+    # CR: a contiguous run of s stragglers that moves by one worker per step
+    (Workload("adv_cr_moving_run", "CR", "lsq", n=8, c=3, N=8 * 256, d=128, lr=0.05, steps=10,
+              policy=POLICY_EXACT, cap=0, seed=29),
+     lambda t, n: [1 if (i - t) % n in (0, 1) else 0 for i in range(n)]),
+    # the real-valued code with worker 5 straggling at every step
+    (Workload("adv_real_persistent", "CR_REAL", "lsq", n=8, c=3, N=8 * 256, d=128, lr=0.02, steps=10,
+              policy=POLICY_EXACT, cap=0, seed=30, code_seed=2),
+     lambda t, n: [1 if i == 5 else 0 for i in range(n)]),
+]
+
+
+@pytest.mark.parametrize("w,pattern", ADVERSARIAL, ids=[a[0].name for a in ADVERSARIAL])
+def test_adversarial_stragglers_match_the_oracle_and_still_store(w, pattern):
+    """The trajectory under a hand-made straggler pattern matches the oracle,
+    and the workers that straggled at the last step still hold, in every slot,
+    the gradient of that slot's partition at the iterate where they last
+    evaluated it (stragglers compute and store; only their coded gradients
+    are left out)."""
+    _announce(w.name)
+    masks = [np.array(pattern(t, w.n), np.uint8) for t in range(w.steps)]
+    X, y, beta0 = make_inputs(w, device="cuda")
+    Xh, yh, bh = _to_host(X, y, beta0)
+    recs_or = oracle_run(w, Xh, yh, bh, masks)
+    sess = gpu_session(w)
+    try:
+        wv = beta0.clone()
+        iterates = []
+        for t, mask in enumerate(masks):
+            iterates.append(wv.cpu().numpy().astype(np.float64))
+            sess.step(X, y, wv, mask, w.lr)
+            assert normwise_error(sess.decoded().cpu().numpy(), recs_or[t].ghat) <= FP32_TOL, t
+            assert normwise_error(wv.cpu().numpy(), recs_or[t].beta) <= FP32_TOL, t
+        place = sess.placement()
+        m = w.m
+        for i in np.flatnonzero(masks[-1]):
+            for l in range(w.c):
+                evaluated = [t for t in range(1, w.steps) if (t - 1) % w.c == l]
+                tau = evaluated[-1] if evaluated else 0
+                k = place[i][l]
+                g = O.partition_gradient(w.model, Xh[k * m:(k + 1) * m].astype(np.float64),
+                                         yh[k * m:(k + 1) * m].astype(np.float64), iterates[tau])
+                err = normwise_error(sess.ring(int(i), l).cpu().numpy(), g)
+                assert err <= FP32_TOL, "worker %d slot %d: %.3g" % (i, l, err)
+    finally:
+        sess.close()
+
+
 def test_unaligned_features_take_the_scalar_path():
     w = Workload("edge_unaligned", "CR", "lsq", n=4, c=2, N=4 * 200, d=256, lr=0.05, steps=6,
                  policy=POLICY_EXACT, cap=1, seed=22)
