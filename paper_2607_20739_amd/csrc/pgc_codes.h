@@ -35,9 +35,6 @@ inline uint64_t step_draw(uint64_t seed, int64_t t, uint64_t j) {
 bool make_mask(uint64_t seed, int64_t t, int policy, int n, int cap, double p,
                uint8_t* out);
 
-// The s x n matrix H (row-major) whose null space holds the real-valued code:
-// uniform entries in [-1, 1) for columns < n-1, last column = minus the row
-// sum accumulated left to right, so H * 1 = 0.
 // One step of the simulated cluster of Sec. VI-B: worker i finishes after
 // compute_seconds + delay_i, delay_i = -mean_delay * ln(1 - u_i) with u_i the
 // draw i of step t; the master proceeds at the (n - s)-th finish.  Writes the
@@ -46,6 +43,9 @@ bool make_mask(uint64_t seed, int64_t t, int policy, int n, int cap, double p,
 bool delay_step(uint64_t seed, int64_t t, int n, int s, double mean_delay, double compute_seconds,
                 uint8_t* mask, double* delays, double* step_seconds);
 
+// The s x n matrix H (row-major) whose null space holds the real-valued code:
+// uniform entries in [-1, 1) for columns < n-1, last column = minus the row
+// sum accumulated left to right, so H * 1 = 0.
 std::vector<double> null_space_generator(uint64_t seed, int s, int n);
 
 // Real-valued cyclic-repetition matrix B (n x n, row-major): row j supported on
