@@ -6,7 +6,8 @@ per-partition gradients of every evaluated partition, the ring write, the
 encode of every worker's coded gradient, the masked decode and the update,
 over the full synthetic dataset resident in HBM.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME | --config K]
+                  [--lr LR] [--seed S] [--steps-log PATH]
 
 Prints one JSON line.  `value` is steps/s; `roofline` is the gradient kernel
 (the dominant one) against the 8 TB/s HBM peak, timed with HIP events around
@@ -147,6 +148,13 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--config", type=int, default=0, metavar="K",
+                    help="run the K-th listed workload instead (1 = the small case, 2 = the default)")
+    ap.add_argument("--lr", type=float, default=None, help="override the workload's learning rate")
+    ap.add_argument("--seed", type=int, default=None, help="override the workload's data and mask seed")
+    ap.add_argument("--steps-log", default="", metavar="PATH",
+                    help="write one JSON line per step of the untimed repeat pass (t, stragglers, "
+                         "survivors, decode scale, step time)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--all-kernel-times", action="store_true",
@@ -161,7 +169,7 @@ def main():
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
     if args.steps < 1 or args.warmup < 1:
@@ -171,9 +179,23 @@ def main():
 
     import torch
     import paper_2607_20739_amd as P
-    from workloads import WORKLOADS, make_inputs
+    from dataclasses import replace
+    from workloads import ORDER, WORKLOADS, make_inputs
 
-    w = WORKLOADS[args.workload]
+    name = args.workload
+    if args.config:
+        if not 1 <= args.config <= len(ORDER):
+            print("--config must be 1..%d" % len(ORDER), file=sys.stderr)
+            return 2
+        name = ORDER[args.config - 1]
+    if name not in WORKLOADS:
+        print("unknown workload %r (known: %s)" % (name, ", ".join(ORDER)), file=sys.stderr)
+        return 2
+    w = WORKLOADS[name]
+    if args.lr is not None:
+        w = replace(w, lr=args.lr)
+    if args.seed is not None:
+        w = replace(w, seed=args.seed)
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         return 1
@@ -233,10 +255,29 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     warmup_step_ms = start.elapsed_time(stop)
+    steps_log = open(args.steps_log, "w") if args.steps_log else None
+
+    def log_step(t, step_ms):
+        survivors, _, scale = sess.decode_coeffs(masks[t])
+        steps_log.write(json.dumps({"t": t, "stragglers": [int(i) for i in masks[t].nonzero()[0]],
+                                    "survivors": [int(i) for i in survivors], "decode_scale": scale,
+                                    "step_ms": step_ms}) + "\n")
+
+    if steps_log:
+        log_step(0, warmup_step_ms)
     for t in range(1, total):
+        if steps_log:
+            start.record(stream)
         sess.step(X, y, w_check, masks[t], w.lr)
+        if steps_log:
+            stop.record(stream)
         sess.decoded()
+        if steps_log:
+            torch.cuda.synchronize()
+            log_step(t, start.elapsed_time(stop))
     torch.cuda.synchronize()
+    if steps_log:
+        steps_log.close()
     reproduced = bool(torch.equal(w_check, wv))
     if not reproduced:
         log("the repeated pass did not reproduce the timed pass's weights bit for bit")
@@ -279,7 +320,7 @@ def main():
         "dtype": "bf16" if w.model == "mlp" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "scheme": w.scheme, "loss": w.model, "n": w.n, "c": w.c,
-                   "N": w.N, "d": w.d, "q": w.q, "lr": w.lr},
+                   "N": w.N, "d": w.d, "q": w.q, "lr": w.lr, "seed": w.seed},
         "samples_per_s": {"unique_rows": rows * steps_per_s, "worker_samples": w.N * steps_per_s},
         "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
         "kernel_ms_per_launch": per_launch,
