@@ -7,7 +7,8 @@ Every HIP and C++ source under csrc/ is compiled with
   -Xclang -target-feature -Xclang -packed-fp32-ops
 (the last pair keeps the compiler from emitting packed fp32 VALU instructions;
 the host pass reports the feature as unknown, which is harmless) and linked
-into paper_2607_20739_amd/libpgc.so next to this file.
+into paper_2607_20739_amd/libpgc.so next to this file, linked against ROCm's
+roctx library for the per-step profiler ranges.
 """
 
 import concurrent.futures
@@ -24,6 +25,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpgc.so")
 SOURCES = sorted(f for f in os.listdir(CSRC) if f.endswith((".cpp", ".hip")))
 ARCH = "gfx950"
+ROCM_LIB = "/opt/rocm/lib"   # librocprofiler-sdk-roctx (per-step profiler ranges)
 
 
 def hipcc():
@@ -54,7 +56,8 @@ def build(verbose=False):
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as pool:
         objs = list(pool.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
+    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs + [
+        "-L" + ROCM_LIB, "-Wl,-rpath," + ROCM_LIB, "-lrocprofiler-sdk-roctx"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("linking libpgc.so failed:\n%s\n%s" % (" ".join(cmd), res.stderr))

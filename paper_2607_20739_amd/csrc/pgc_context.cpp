@@ -1,6 +1,7 @@
 // C ABI of the PGC step (include/pgc.h): context, validation, workspace
 // layout and the per-step launch sequence.
 #include <hip/hip_runtime_api.h>
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include <algorithm>
 #include <cstring>
@@ -645,20 +646,23 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
   const int plane_first = fr ? 0 : o;
   const int plane_count = (!fr && warm) ? c : 1;
 
-  int st;
+  bool aligned16 = false;
   if (ctx->cfg.model == PGC_MLP) {
     if (reinterpret_cast<uintptr_t>(X) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
         reinterpret_cast<uintptr_t>(w) % 4 != 0)
       return fail(ctx, PGC_EINVAL, "MLP: X must be 16-byte aligned, y and w 4-byte aligned");
-    st = mlp_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
   } else {
-    const bool aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 &&
-                           reinterpret_cast<uintptr_t>(w) % 16 == 0;
+    aligned16 = reinterpret_cast<uintptr_t>(X) % 16 == 0 && reinterpret_cast<uintptr_t>(w) % 16 == 0;
     if (!pgc::linear_grad_shape(static_cast<int>(ctx->d), aligned16).supported)
       return fail(ctx, PGC_EINVAL, "d = " + std::to_string(ctx->d) +
                                        " needs d % 4 == 0 and 16-byte aligned X and w");
-    st = linear_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
   }
+  // A host-side range per step, for profilers that record roctx markers.
+  roctxRangePushA(warm ? "pgc_step (warm-up)" : "pgc_step");
+  const int st = ctx->cfg.model == PGC_MLP
+                     ? mlp_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count)
+                     : linear_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
+  roctxRangePop();
   if (st != PGC_OK) return st;
   ctx->t += 1;
   return PGC_OK;
