@@ -92,7 +92,13 @@ def read_traffic(workload, bound):
 
 
 def cpu_baseline(w, X, y, beta0, budget_s):
-    """The oracle, as it stands, on the host over the first steps of the same run."""
+    """The oracle, as it stands, on the host over the first steps of the same run.
+
+    The oracle runs the whole workload when its fp64 copy of X fits in 8 GiB.
+    Larger linear workloads run on a prefix of every partition's rows (the
+    same n, c, d, masks and lr), with the rate scaled to the full row count:
+    their step is per-row gradient work plus an encode / decode over n c d
+    values, well under 1% of a full step at those sizes."""
     from threadpoolctl import threadpool_info
     from oracle import pgc_oracle as O
     from oracle import rng as R
@@ -101,32 +107,51 @@ def cpu_baseline(w, X, y, beta0, budget_s):
     if w.scheme == "CR_REAL":
         B = O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
     max_steps = 100000
-    Xh, yh, bh = X.float().cpu().numpy(), y.cpu().numpy(), beta0.cpu().numpy()
+    m = w.N // w.n
     shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
+    rows = m if w.N * w.d * 8 <= (8 << 30) else max(1, (4 << 30) // (w.n * w.d * 8))
+    Xs = X.view(w.n, m, w.d)[:, :rows].reshape(w.n * rows, w.d).float().cpu().numpy()
+    ys = y.view(w.n, m)[:, :rows].reshape(-1).cpu().numpy()
+    bs = beta0.cpu().numpy()
 
     def run(steps):
         masks = [R.straggler_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(steps)]
         t0 = time.perf_counter()
-        O.run(schemes[w.scheme], w.model, w.n, w.c, Xh, yh, bh, w.lr, masks, B=B, shape=shape,
+        O.run(schemes[w.scheme], w.model, w.n, w.c, Xs, ys, bs, w.lr, masks, B=B, shape=shape,
               keep_coded=False, keep_alpha=False)
         return time.perf_counter() - t0
 
-    # Size the sample from two probes (10 and 30 steps): their difference is
-    # the marginal cost of a step, the rest the one-time setup (the oracle's
-    # fp64 copy of X).
-    # The estimate is floored at a quarter of the longer probe's average, so a
-    # noisy difference cannot inflate the sample.
-    t_short, t_long = run(10), run(30)
-    per_step = max((t_long - t_short) / 20, t_long / 30 / 4, 1e-6)
-    setup = max(t_short - 10 * per_step, 0.0)
-    steps = int(max(2, min(max_steps, (budget_s - setup) / per_step)))
-    log("oracle: ~%.1f ms per step, ~%.1f s setup; timing %d steps" % (per_step * 1e3, setup, steps))
-    elapsed = run(steps)
+    # Marginal cost of a step from runs of 1 and 3 steps (their difference
+    # cancels the one-time fp64 copy of X).
+    t_one, t_three = run(1), run(3)
+    per_step = max((t_three - t_one) / 2, 1e-6)
+    if per_step * 30 > budget_s:
+        # Slow steps (the MLP at full size): report that marginal rate.
+        steps, elapsed = 2, t_three - t_one
+        log("oracle: ~%.1f s per step from runs of 1 and 3 steps" % per_step)
+        what = ("fp64 numpy oracle, marginal cost of a step from runs of steps t=0 and t=0..2 of the "
+                "same workload and masks (%.1f s and %.1f s wall)" % (t_one, t_three))
+    else:
+        # Size the sample from two probes (10 and 30 steps): their difference is
+        # the marginal cost of a step, the rest the one-time setup (the oracle's
+        # fp64 copy of X).  The estimate is floored at a quarter of the longer
+        # probe's average, so a noisy difference cannot inflate the sample.
+        t_short, t_long = run(10), run(30)
+        per_step = max((t_long - t_short) / 20, t_long / 30 / 4, 1e-6)
+        setup = max(t_short - 10 * per_step, 0.0)
+        steps = int(max(2, min(max_steps, (budget_s - setup) / per_step)))
+        log("oracle: %d of %d rows per partition, ~%.1f ms per step, ~%.1f s setup; timing %d steps"
+            % (rows, m, per_step * 1e3, setup, steps))
+        elapsed = run(steps)
+        what = ("fp64 numpy oracle over steps t=0..%d of the same workload and masks (%.1f s wall, "
+                "including its one-time fp64 copy of X)" % (steps - 1, elapsed))
     threads = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
     cores = min(max(threads) if threads else 1, len(os.sched_getaffinity(0)))
-    return {"value": steps / elapsed, "unit": "steps/s", "cores": cores, "kind": "oracle",
-            "sample": "fp64 numpy oracle over steps t=0..%d of the same workload and masks "
-                      "(%.1f s wall, including its one-time fp64 copy of X)" % (steps - 1, elapsed)}
+    if rows < m:
+        what += ("; run on the first %d of the %d rows of every partition, rate scaled by %d/%d"
+                 % (rows, m, rows, m))
+    return {"value": steps / elapsed * rows / m, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": what}
 
 
 def copy_calibration(nbytes):
@@ -146,7 +171,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before the timed ones (default: at least 20 and at least "
+                         "0.25 s of steps, so the GPU's clocks have ramped up)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--config", type=int, default=0, metavar="K",
                     help="run the K-th listed workload instead (1 = the small case, 2 = the default)")
@@ -172,7 +199,7 @@ def main():
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
-    if args.steps < 1 or args.warmup < 1:
+    if args.steps < 1 or (args.warmup is not None and args.warmup < 1):
         print("--steps and --warmup must be >= 1 (the first warm-up step is the pipeline fill t = 0)",
               file=sys.stderr)
         return 2
@@ -203,15 +230,29 @@ def main():
     torch.cuda.set_device(dev)
     log("workload %s: generating inputs" % w.name)
     X, y, beta0 = make_inputs(w, device=dev)
-    total = args.warmup + args.steps
-    masks = [P.pgc_make_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(total)]
+    masks = []
+
+    def mask(t):
+        while len(masks) <= t:
+            masks.append(P.pgc_make_mask(w.mask_seed, len(masks), w.policy, w.n, w.cap, w.p))
+        return masks[t]
     sess = P.PGCSession(w.scheme, w.n, w.c, w.model, w.N, w.d, hidden=w.hidden, classes=w.classes,
                         code_seed=w.code_seed, device=dev)
     wv = beta0.clone()
-    log("warm-up: %d steps (t = 0 fills the pipeline)" % args.warmup)
-    for t in range(args.warmup):
-        sess.step(X, y, wv, masks[t], w.lr)
+    if args.warmup is not None:
+        warmup = args.warmup
+        for t in range(warmup):
+            sess.step(X, y, wv, mask(t), w.lr)
+    else:
+        warmup, t0 = 0, time.perf_counter()
+        while warmup < 20 or time.perf_counter() - t0 < 0.25:
+            for _ in range(20):
+                sess.step(X, y, wv, mask(warmup), w.lr)
+                warmup += 1
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
+    log("warm-up: %d steps (t = 0 fills the pipeline)" % warmup)
+    total = warmup + args.steps
 
     stream = torch.cuda.current_stream(dev)
     start = torch.cuda.Event(enable_timing=True)
@@ -225,8 +266,8 @@ def main():
     P.pgc_set_timing_period(sess.ctx, max(1, args.time_every))
     torch.cuda.synchronize()
     start.record(stream)
-    for t in range(args.warmup, total):
-        sess.step(X, y, wv, masks[t], w.lr)
+    for t in range(warmup, total):
+        sess.step(X, y, wv, mask(t), w.lr)
     stop.record(stream)
     torch.cuda.synchronize()
     elapsed_ms = start.elapsed_time(stop)
@@ -251,15 +292,15 @@ def main():
     w_check = beta0.clone()
     torch.cuda.synchronize()
     start.record(stream)
-    sess.step(X, y, w_check, masks[0], w.lr)
+    sess.step(X, y, w_check, mask(0), w.lr)
     stop.record(stream)
     torch.cuda.synchronize()
     warmup_step_ms = start.elapsed_time(stop)
     steps_log = open(args.steps_log, "w") if args.steps_log else None
 
     def log_step(t, step_ms):
-        survivors, _, scale = sess.decode_coeffs(masks[t])
-        steps_log.write(json.dumps({"t": t, "stragglers": [int(i) for i in masks[t].nonzero()[0]],
+        survivors, _, scale = sess.decode_coeffs(mask(t))
+        steps_log.write(json.dumps({"t": t, "stragglers": [int(i) for i in mask(t).nonzero()[0]],
                                     "survivors": [int(i) for i in survivors], "decode_scale": scale,
                                     "step_ms": step_ms}) + "\n")
 
@@ -268,7 +309,7 @@ def main():
     for t in range(1, total):
         if steps_log:
             start.record(stream)
-        sess.step(X, y, w_check, masks[t], w.lr)
+        sess.step(X, y, w_check, mask(t), w.lr)
         if steps_log:
             stop.record(stream)
         sess.decoded()
@@ -312,7 +353,7 @@ def main():
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
