@@ -132,7 +132,9 @@ int pgc_workspace_bytes(const pgc_ctx* ctx, size_t* bytes);
 /* Bind caller-owned device memory of at least pgc_workspace_bytes bytes,
  * 256-byte aligned, used until the context is destroyed or rebound.  It holds
  * the gradient ring, the coded and decoded gradients and per-block partial
- * sums.  Uploads the encoding table with a synchronous copy.  Resets t to 0. */
+ * sums.  Synchronises the context stream (work enqueued before may still use
+ * the old workspace), then uploads the encoding table with a synchronous copy.
+ * Resets t to 0. */
 int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes);
 
 /* One PGC step at the context's current step t, then t += 1.

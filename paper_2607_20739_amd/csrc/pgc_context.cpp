@@ -169,8 +169,10 @@ int resolve_timing(pgc_ctx* ctx, bool wait) {
     if (wait) {
       hipError_t e = hipEventSynchronize(tm.stop);
       if (e != hipSuccess) return device_fail(ctx, e, "hipEventSynchronize");
-    } else if (hipEventQuery(tm.stop) != hipSuccess) {
-      break;
+    } else {
+      const hipError_t q = hipEventQuery(tm.stop);
+      if (q == hipErrorNotReady) break;
+      if (q != hipSuccess) return device_fail(ctx, q, "hipEventQuery");
     }
     float ms = 0.f;
     hipError_t e = hipEventElapsedTime(&ms, tm.start, tm.stop);
@@ -198,18 +200,30 @@ int timed_launch(pgc_ctx* ctx, int kernel, const char* what, Fn fn) {
       ctx->spare.pop_back();
     } else {
       hipError_t e = hipEventCreate(&tm.start);
-      if (e == hipSuccess) e = hipEventCreate(&tm.stop);
+      if (e == hipSuccess) {
+        e = hipEventCreate(&tm.stop);
+        if (e != hipSuccess) (void)hipEventDestroy(tm.start);
+      }
       if (e != hipSuccess) return device_fail(ctx, e, "hipEventCreate");
     }
     tm.kernel = kernel;
     hipError_t e = hipEventRecord(tm.start, ctx->stream);
-    if (e != hipSuccess) return device_fail(ctx, e, "hipEventRecord");
+    if (e != hipSuccess) {
+      ctx->spare.push_back(tm);
+      return device_fail(ctx, e, "hipEventRecord");
+    }
   }
   hipError_t e = fn();
-  if (e != hipSuccess) return device_fail(ctx, e, what);
+  if (e != hipSuccess) {
+    if (timed) ctx->spare.push_back(tm);   // the pair is reused; its start is simply re-recorded
+    return device_fail(ctx, e, what);
+  }
   if (timed) {
     e = hipEventRecord(tm.stop, ctx->stream);
-    if (e != hipSuccess) return device_fail(ctx, e, "hipEventRecord");
+    if (e != hipSuccess) {
+      ctx->spare.push_back(tm);
+      return device_fail(ctx, e, "hipEventRecord");
+    }
     ctx->pending.push_back(tm);
   }
   return PGC_OK;
@@ -345,12 +359,16 @@ int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes) {
     return fail(ctx, PGC_EINVAL, "workspace must be 256-byte aligned");
   if (bytes < ctx->ws_need)
     return fail(ctx, PGC_EINVAL, "workspace too small: need " + std::to_string(ctx->ws_need) + " bytes");
+  // Work already enqueued on the context stream may still read the old
+  // workspace (a rebind of the same memory rewrites the code table below).
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return device_fail(ctx, e, "hipStreamSynchronize");
   ctx->ws = static_cast<char*>(dev_workspace);
   ctx->ws_bytes = bytes;
   ctx->t = 0;
   if (!ctx->coef.empty()) {
-    hipError_t e = hipMemcpy(ctx->ws + ctx->off_coef, ctx->coef.data(),
-                             sizeof(double) * ctx->coef.size(), hipMemcpyHostToDevice);
+    e = hipMemcpy(ctx->ws + ctx->off_coef, ctx->coef.data(), sizeof(double) * ctx->coef.size(),
+                  hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       ctx->ws = nullptr;
       return device_fail(ctx, e, "uploading the encoding table");
