@@ -20,6 +20,17 @@ def normwise_error(a, b):
     return float(np.max(np.abs(a - b)) / scale) if scale > 0 else float(np.max(np.abs(a - b)))
 
 
+def elementwise_error(a, b, floor=1e-3):
+    """max_i |a_i - b_i| / max(|b_i|, floor * max_j |b_j|): the elementwise
+    relative error, with an absolute floor so that entries near zero do not
+    make it meaningless.  Reported beside the normwise bar, not gated."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    scale = np.maximum(np.abs(b), floor * np.max(np.abs(b)))
+    scale = np.where(scale > 0, scale, 1.0)
+    return float(np.max(np.abs(a - b) / scale))
+
+
 def oracle_masks(w, steps=None):
     steps = w.steps if steps is None else steps
     return [R.straggler_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(steps)]

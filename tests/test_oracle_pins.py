@@ -544,3 +544,14 @@ def test_is_sgd_rejects_an_empty_survivor_set_and_c_above_one():
         O.decode_weights(O.IS_SGD, 4, 1, [])
     with pytest.raises(ValueError):
         O.placement(O.IS_SGD, 4, 2)
+
+
+def test_elementwise_error_with_floor():
+    """The reported elementwise metric: relative per entry, with entries below
+    1e-3 of the largest judged against that floor instead of themselves."""
+    from _parity import elementwise_error
+    b = np.array([10.0, 1e-9, -2.0])
+    assert elementwise_error(b, b) == 0.0
+    assert elementwise_error(b * (1 + 1e-6), b) == pytest.approx(1e-6)
+    # An absolute error of 1e-6 on the tiny entry is measured against 1e-3 * 10.
+    assert elementwise_error(b + np.array([0.0, 1e-6, 0.0]), b) == pytest.approx(1e-4)
