@@ -141,7 +141,7 @@ void compute_layout(pgc_ctx* ctx) {
     ctx->off_w1t = take(2 * static_cast<size_t>(hidden * ctx->kpad));
     ctx->off_w2t = take(2 * static_cast<size_t>(pgc::kMlpMaxClasses * hidden));
     ctx->off_w2p = take(2 * static_cast<size_t>(hidden * pgc::kMlpMaxClasses));
-    ctx->off_h = take(2 * static_cast<size_t>(n) * ctx->m * hidden);
+    ctx->off_h = take(2 * static_cast<size_t>(n) * ctx->m_pad * hidden);
     ctx->off_dz1 = take(2 * static_cast<size_t>(n) * hidden * ctx->m_pad);
     ctx->off_partials = take(sizeof(float) * static_cast<size_t>(head_blocks * ctx->pstride));
   } else {
@@ -549,6 +549,7 @@ int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::De
   fw.b1 = w + w1;
   fw.H = H;
   fw.m = ctx->m;
+  fw.m_pad = ctx->m_pad;
   fw.d_in = d_in;
   fw.kpad = static_cast<int32_t>(ctx->kpad);
   fw.hidden = hidden;

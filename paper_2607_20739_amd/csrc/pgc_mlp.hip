@@ -220,8 +220,8 @@ void mlp_forward_kernel(MlpForwardArgs a) {
   }
 
   // Epilogue: bias and ReLU, then the 256 x 256 bf16 tile goes through LDS
-  // (row r's 16-byte chunk cc at slot cc ^ (r & 31)) so that H leaves in whole
-  // 512-byte row segments, 16 bytes per lane.
+  // (row r's 16-byte chunk cc at slot cc ^ (r & 31)) so that H leaves in its
+  // blocked layout, 1 KiB of contiguous memory per store instruction.
   lds_barrier();   // every wave is done reading the operand buffers
   bf16* out = &smem[0][0][0];
 #pragma unroll
@@ -240,16 +240,24 @@ void mlp_forward_kernel(MlpForwardArgs a) {
     }
   }
   lds_barrier();
-  bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * a.hidden + h0;
-  const int cc = tid & 31;
+  // The tile is 16 row blocks x 2 hidden blocks of 4 KiB; chunk q of a block
+  // is fragment slice q / 64, lane q % 64 (row q % 16, 8-unit group (q / 16) % 4).
+  const int64_t hblocks = a.hidden / 128;
+  bf16* Hb = a.H + ((static_cast<int64_t>(e) * (a.m_pad / 16) + r0 / 16) * hblocks + h0 / 128) * 2048;
 #pragma unroll 4
-  for (int r = tid >> 5; r < kFwBM; r += kFwThreads / 32) {
+  for (int it = 0; it < kFwBM * kFwBN / 8 / kFwThreads; ++it) {
+    const int q = it * kFwThreads + tid;
+    const int blk = q >> 8, rbl = blk >> 1, hbl = blk & 1, within = q & 255;
+    const int r = rbl * 16 + (within & 15);
+    const int cc = hbl * 16 + (within >> 6) * 4 + ((within >> 4) & 3);
     const int64_t row = r0 + r;
-    if (row < a.m)
+    if (row < a.m_pad) {
+      const bf16x8 v = row < a.m ? *reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)])
+                                 : bf16x8{};
       // H (2 GB per step) cannot stay in the caches until the head reads it:
       // streaming stores keep it from evicting the reused X and W1^T tiles.
-      __builtin_nontemporal_store(*reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)]),
-                                  reinterpret_cast<bf16x8*>(Hp + row * a.hidden + cc * 8));
+      __builtin_nontemporal_store(v, reinterpret_cast<bf16x8*>(Hb + (rbl * hblocks + hbl) * 2048 + within * 8));
+    }
   }
 }
 
@@ -285,7 +293,9 @@ void mlp_head_kernel(MlpHeadArgs a) {
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
   const int hw0 = wave * kHeadCols;
   const int64_t hidden = a.hidden;
-  const bf16* Hp = a.H + static_cast<int64_t>(e) * a.m * hidden;
+  // This wave's 4 KiB block of H for row block rb starts at Hw + rb * hblocks * 2048.
+  const int64_t hblocks = hidden / 128;
+  const bf16* Hw = a.H + (static_cast<int64_t>(e) * (a.m_pad / 16) * hblocks + wave) * 2048;
   const int32_t* yp = a.y + part * a.m;
   bf16* dz1 = a.dZ1 + mlp_dz1_index(a.m_pad, a.hidden, e, 0, 0);
   const int64_t rbeg = static_cast<int64_t>(blockIdx.x) * a.rows_per_block;
@@ -314,15 +324,15 @@ void mlp_head_kernel(MlpHeadArgs a) {
   // them wait for the prefetched tiles too: loads complete in order).
   bf16x8 ha[4], hb[4];
   int la[4], lb[4];
-  // Every fetch issues the same loads on every path (rows past the partition
-  // load its last row), and the values are only masked where a tile uses them,
-  // so the compiler's waits for a register set count exactly the loads issued
-  // after it.
+  // Every fetch issues the same loads on every path (H rows m .. m_pad - 1 are
+  // zeros; labels past the partition read its last row), and the values are
+  // only masked where a tile uses them, so the compiler's waits for a register
+  // set count exactly the loads issued after it.  Slice ks of the block is
+  // 1 KiB in lane order: row r0 + lr, columns hw0 + 32 ks + 8 lg .. + 7.
   auto fetch_h = [&](int64_t r0, bf16x8* dst, int* lab) {
-    const int64_t row = r0 + lr;
-    const int64_t src = row < a.m ? row : a.m - 1;
+    const bf16* blk = Hw + (r0 / 16) * hblocks * 2048;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) dst[ks] = load_vec<bf16x8>(Hp + src * hidden + hw0 + ks * 32 + lg * 8);
+    for (int ks = 0; ks < 4; ++ks) dst[ks] = load_vec<bf16x8>(blk + ks * 512 + lane * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t lrow = r0 + lg * 4 + i;
