@@ -113,11 +113,6 @@ hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s);
 //   H[((((e * m_pad / 16 + rb) * hidden / 128 + hb) * 4 + s) * 64 + 16 g + i) * 8 + j].
 // A (16-row, 128-unit) block is 4 KiB of contiguous memory, and for each s the
 // 64 lanes of a head wave read 1 KiB of it in lane order.
-__host__ __device__ inline int64_t mlp_h_index(int64_t m_pad, int32_t hidden, int32_t e, int64_t r, int32_t h) {
-  const int32_t hh = h % 128;
-  return ((((static_cast<int64_t>(e) * (m_pad / 16) + r / 16) * (hidden / 128) + h / 128) * 4 + hh / 32) * 64 +
-          16 * ((hh % 32) / 8) + r % 16) * 8 + hh % 8;
-}
 
 // H(e; r, h) = bf16(relu(X[k*m + r] . W1[:, h] + b1[h])) for each evaluated
 // partition k = e * part_stride + part_offset, e < n_eval, r < m, in the
