@@ -1,0 +1,78 @@
+"""Host-side checks of bench.py: its argument guards, its algorithmic-work
+accounting, and when it reports measured HBM traffic.  No GPU needed."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from workloads import ORDER, WORKLOADS  # noqa: E402
+
+
+def run_bench(*args):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args],
+                          capture_output=True, text=True, timeout=120)
+
+
+def test_bench_measures_one_gpu_only():
+    res = run_bench("--gpus", "2")
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+    assert res.stdout == ""
+
+
+def test_bench_rejects_an_empty_timed_region():
+    res = run_bench("--steps", "0")
+    assert res.returncode == 2
+    assert "--steps" in res.stderr
+
+
+@pytest.mark.parametrize("name", [n for n in ORDER if WORKLOADS[n].model != "mlp"])
+def test_linear_step_bytes_follow_the_per_row_accounting(name):
+    w = WORKLOADS[name]
+    # Each evaluated row: d fp32 features and one fp32 label, read once; plus w.
+    # FR evaluates one partition per group (N / c rows); CR every partition.
+    rows = w.N // w.c if w.scheme == "FR" else w.N
+    grad, step = bench.algorithmic_bytes(w)
+    assert grad == rows * (4 * w.d + 4) + 4 * w.d
+    assert step > grad
+    # The rest of the step (ring, coded words, w) is under 1% of the stream
+    # except for the cache-resident d = 64 case.
+    if w.d >= 1024:
+        assert (step - grad) < 0.01 * grad
+
+
+def test_mlp_gemm_flops_are_two_per_multiply_add():
+    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+    assert bench.mlp_gemm_flops(w) == 2.0 * 1048576 * 784 * 1024
+
+
+def test_traffic_is_reported_only_for_the_kernel_source_it_was_measured_on(monkeypatch):
+    with open(bench.TRAFFIC_FILE) as f:
+        data = json.load(f)
+    name = "crreal_lsq_n8_c3_d1024"
+    entry = data[name]
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda bound: entry["kernel_source_sha256_16"])
+    assert bench.read_traffic(name, "hbm") == entry["bytes_per_launch"]
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda bound: "0" * 16)
+    assert bench.read_traffic(name, "hbm") is None
+    assert bench.read_traffic("no_such_workload", "hbm") is None
+
+
+def test_recorded_traffic_covers_the_algorithmic_bytes():
+    """Counters read at least what the kernel must stream (X and y once)."""
+    with open(bench.TRAFFIC_FILE) as f:
+        data = json.load(f)
+    for name, entry in data.items():
+        w = WORKLOADS[name]
+        if w.model == "mlp":
+            must_read = w.N * w.d * 2   # bf16 X
+        else:
+            must_read = bench.algorithmic_bytes(w)[0] - 4 * w.d
+        assert entry["read_bytes"] >= 0.999 * must_read, name
