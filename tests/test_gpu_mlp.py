@@ -78,13 +78,34 @@ SMALL = [
     # the real-valued code on the MLP
     Workload("mlp_real_code", "CR_REAL", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=34, hidden=256, classes=10, code_seed=3),
+    # the smallest d_in (one 16-byte chunk per row: the forward's one K step is 56 columns of
+    # padding, the weight gradient's one feature tile 8 features wide) with the most classes
+    Workload("mlp_cr_min_din_max_classes", "CR", "mlp", n=4, c=2, N=4 * 64, d=8, lr=0.05, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=37, hidden=256, classes=16),
 ]
+
+# One class: the softmax is exactly 1, so dZ2, every gradient and every update are exactly zero.
+ONE_CLASS = Workload("mlp_cr_one_class", "CR", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.05, steps=4,
+                     policy=POLICY_EXACT, cap=1, seed=37, hidden=256, classes=1)
 
 
 @pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
 def test_small_mlp_trajectory_matches_oracle(w):
     _announce("%s N=%d d_in=%d hidden=%d" % (w.name, w.N, w.d, w.hidden))
     _check_trajectory(w)
+
+
+def test_one_class_mlp_has_exactly_zero_gradients():
+    w = ONE_CLASS
+    _announce("%s N=%d d_in=%d hidden=%d classes=1" % (w.name, w.N, w.d, w.hidden))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = gpu_masks(w)
+    recs, w_final = gpu_run(w, X, y, beta0, masks)
+    for t, g in enumerate(recs):
+        assert np.all(g["ghat"] == 0.0), "step %d: nonzero decoded gradient" % t
+    assert torch.equal(w_final.cpu(), beta0.cpu())
+    ref = oracle_run(w, *_host_inputs(X, y, beta0), oracle_masks(w))
+    assert all(np.all(o.ghat == 0.0) for o in ref)
 
 
 def test_mlp_workload_shape_trajectory_matches_oracle():
