@@ -230,6 +230,34 @@ def test_adversarial_stragglers_match_the_oracle_and_still_store(w, pattern):
         sess.close()
 
 
+# lr = 0: every ring copy is g_k(w(0)), so the two exact decoders (FR, and the
+# real-valued code of Sec. V-A) must return the full-batch mean gradient
+# (1/N) sum_r slope(x_r . w(0), y_r) x_r at every step, under every straggler set
+# drawn, and w stays w(0) bit for bit.  The reference is that definition written
+# out in fp64, not the oracle's pipeline.
+ZERO_LR = [
+    Workload("zero_lr_fr_logistic", "FR", "logistic", n=6, c=3, N=6 * 700, d=300, lr=0.0, steps=7,
+             policy=POLICY_EXACT, cap=2, seed=43),
+    Workload("zero_lr_real_lsq", "CR_REAL", "lsq", n=8, c=3, N=8 * 600, d=256, lr=0.0, steps=7,
+             policy=POLICY_UNIFORM_COUNT, cap=2, seed=44, code_seed=2),
+]
+
+
+@pytest.mark.parametrize("w", ZERO_LR, ids=[w.name for w in ZERO_LR])
+def test_zero_learning_rate_decodes_the_full_batch_gradient(w):
+    _announce("%s N=%d d=%d lr=0" % (w.name, w.N, w.d))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    recs, w_final = gpu_run(w, X, y, beta0, gpu_masks(w))
+    Xh, yh, bh = (t.double().cpu().numpy() for t in (X, y, beta0))
+    z = Xh @ bh
+    slope = 1.0 / (1.0 + np.exp(-z)) - yh if w.model == "logistic" else z - yh
+    full = Xh.T @ slope / w.N
+    for t, g in enumerate(recs):
+        e = normwise_error(g["ghat"], full)
+        assert e <= FP32_TOL, "step %d: error %.3g against the full-batch gradient" % (t, e)
+    assert torch.equal(w_final, beta0)
+
+
 def test_unaligned_features_take_the_scalar_path():
     w = Workload("edge_unaligned", "CR", "lsq", n=4, c=2, N=4 * 200, d=256, lr=0.05, steps=6,
                  policy=POLICY_EXACT, cap=1, seed=22)
