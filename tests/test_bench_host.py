@@ -76,3 +76,13 @@ def test_recorded_traffic_covers_the_algorithmic_bytes():
         else:
             must_read = bench.algorithmic_bytes(w)[0] - 4 * w.d
         assert entry["read_bytes"] >= 0.999 * must_read, name
+
+
+def test_cpu_baseline_reports_the_oracle_rate_on_a_bounded_sample():
+    from workloads import make_inputs
+    w = WORKLOADS["fr_logistic_n4_c2_d64"]
+    X, y, beta0 = make_inputs(w)
+    res = bench.cpu_baseline(w, X, y, beta0, budget_s=1.0)
+    assert res["kind"] == "oracle" and res["unit"] == "steps/s"
+    assert res["value"] > 0 and res["cores"] >= 1
+    assert "oracle" in res["sample"] and "rows" not in res["sample"]   # small X: every row is used
