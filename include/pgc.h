@@ -140,6 +140,9 @@ int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes);
 /* One PGC step at the context's current step t, then t += 1.
  *   X    device; row-major N x d_in: fp32 (linear models) or bf16 bit patterns (MLP).
  *   y    device; N labels: fp32 {0,1} (logistic), fp32 (least squares), int32 class (MLP).
+ *        MLP classes lie in [0, classes); the kernels only compare a label with
+ *        class indices, so another value indexes no memory: its row's one-hot
+ *        target is all zero.
  *   w    device; fp32 parameter vector of length d, updated in place:
  *        w <- w - lr * ghat, ghat the decoded gradient (Sec. III).  MLP layout:
  *        W1[d_in][hidden] row-major, b1[hidden], W2[hidden][classes], b2[classes].
