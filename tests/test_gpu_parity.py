@@ -145,6 +145,9 @@ BASELINES = [
               policy=POLICY_UNIFORM_COUNT, cap=11, seed=44), True),
     (Workload("is_sgd_mlp", "IS_SGD", "mlp", n=4, c=1, N=4 * 64, d=64, lr=0.05, steps=5,
               policy=POLICY_EXACT, cap=2, seed=45, hidden=256, classes=10), True),
+    # gradient coding on the MLP: every step takes the warm-up path (all c slots at w)
+    (Workload("gc_cr_mlp", "CR", "mlp", n=4, c=2, N=4 * 96, d=64, lr=0.05, steps=5,
+              policy=POLICY_EXACT, cap=1, seed=50, hidden=256, classes=10), False),
     # the delay model's stragglers: the s workers with the largest delay draws
     (Workload("delay_cr_logistic_n12_c3", "CR", "logistic", n=12, c=3, N=12 * 256, d=768, lr=0.1, steps=10,
               policy=POLICY_SLOWEST, cap=2, seed=46), True),
