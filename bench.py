@@ -4,16 +4,20 @@
 One "step" is one pipelined PGC step (t >= 1) of the whole hot path: the
 per-partition gradients of every evaluated partition, the ring write, the
 encode of every worker's coded gradient, the masked decode and the update,
-over the full synthetic dataset resident in HBM.
+over the full synthetic dataset resident in HBM.  The default workload is the
+largest: PGC-CR (Sec. V-B), logistic regression, n = 128, c = 8, d = 8192,
+N = 2,097,152 rows (64 GiB of fp32 features).
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME | --config K]
-                  [--lr LR] [--seed S] [--steps-log PATH]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--repeat R]
+                  [--workload NAME | --config K] [--lr LR] [--seed S] [--steps-log PATH]
 
-Prints one JSON line.  `value` is steps/s; `roofline` is the gradient kernel
-(the dominant one) against the 8 TB/s HBM peak, timed with HIP events around
-one in every --time-every of its launches inside the timed region (an event
-pair adds ~6 us to the step it brackets); `cpu_baseline` is the fp64 oracle on
-the host cores over a bounded sample of the same workload.
+Prints one JSON line.  `value` is steps/s, the median of R timed passes of K
+steps each; `roofline` is the gradient kernel (the dominant one) against the
+8 TB/s HBM peak, timed with HIP events around its launches inside the timed
+passes (every launch, or one in --time-every when there are more than 100 of
+them; an event pair adds ~6 us to the step it brackets), with the whole step's
+fraction beside it; `cpu_baseline` is the fp64 oracle on the host cores over a
+bounded sample of the same workload.
 """
 
 import argparse
@@ -28,7 +32,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-DEFAULT_WORKLOAD = "crreal_lsq_n8_c3_d1024"
+DEFAULT_WORKLOAD = "cr_logistic_n128_c8_d8192"
+# Timed launches of the dominant kernel to aim for when --time-every is not given.
+TIMED_LAUNCH_TARGET = 100
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {"hbm": os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_linear.hip"),
                   "mfma": os.path.join(ROOT, "paper_2607_20739_amd", "csrc", "pgc_mlp.hip")}
@@ -167,28 +173,55 @@ def copy_calibration(nbytes):
     return 0
 
 
+def oracle_errors(w, X, y, beta0, masks, recs):
+    """Per-step normwise errors of the decoded gradient and the weights of the
+    repeat pass against the oracle run on the same inputs and masks (CPU)."""
+    import numpy as np
+    from oracle import pgc_oracle as O
+    from oracle import rng as R
+    schemes = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
+    B = None
+    if w.scheme == "CR_REAL":
+        B = O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
+    shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
+    ref = O.run(schemes[w.scheme], w.model, w.n, w.c, X.float().cpu().numpy(), y.cpu().numpy(),
+                beta0.cpu().numpy(), w.lr, masks, B=B, shape=shape, keep_coded=False, keep_alpha=False)
+
+    def err(a, b):
+        scale = np.max(np.abs(b))
+        diff = np.max(np.abs(np.asarray(a, np.float64) - b))
+        return float(diff / scale) if scale > 0 else float(diff)
+    return [(err(g, o.ghat), err(wv, o.beta)) for (g, wv), o in zip(recs, ref)]
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps per pass (default: about 1 s of steps, between 20 and 1000)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps before the timed ones (default: at least 20 and at least "
                          "0.25 s of steps, so the GPU's clocks have ramped up)")
+    ap.add_argument("--repeat", type=int, default=3,
+                    help="timed passes of --steps steps each; value is their median")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--config", type=int, default=0, metavar="K",
-                    help="run the K-th listed workload instead (1 = the small case, 2 = the default)")
+                    help="run the K-th listed workload instead (1 = the small case, 5 = the default)")
     ap.add_argument("--lr", type=float, default=None, help="override the workload's learning rate")
     ap.add_argument("--seed", type=int, default=None, help="override the workload's data and mask seed")
     ap.add_argument("--steps-log", default="", metavar="PATH",
                     help="write one JSON line per step of the untimed repeat pass (t, stragglers, "
-                         "survivors, decode scale, step time)")
+                         "survivors, decode scale, step time, and on workloads whose fp64 copy fits "
+                         "in 2 GiB the normwise errors of ghat and w against the oracle)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--all-kernel-times", action="store_true",
                     help="time every kernel with HIP events (adds event overhead to the step)")
-    ap.add_argument("--time-every", type=int, default=10,
+    ap.add_argument("--time-every", type=int, default=None,
                     help="bracket one launch in this many of each timed kernel with HIP events "
-                         "(an event pair costs ~6 us of step time)")
+                         "(an event pair costs ~6 us of step time; default: every launch when the "
+                         "timed passes hold at most %d, else enough to time about that many)"
+                         % TIMED_LAUNCH_TARGET)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 20 times and exit "
                          "(a known-size reference for the HBM byte counters)")
@@ -199,9 +232,10 @@ def main():
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
-    if args.steps < 1 or (args.warmup is not None and args.warmup < 1):
-        print("--steps and --warmup must be >= 1 (the first warm-up step is the pipeline fill t = 0)",
-              file=sys.stderr)
+    if ((args.steps is not None and args.steps < 1) or (args.warmup is not None and args.warmup < 1)
+            or args.repeat < 1):
+        print("--steps, --warmup and --repeat must be >= 1 (the first warm-up step is the pipeline "
+              "fill t = 0)", file=sys.stderr)
         return 2
 
     import torch
@@ -239,20 +273,28 @@ def main():
     sess = P.PGCSession(w.scheme, w.n, w.c, w.model, w.N, w.d, hidden=w.hidden, classes=w.classes,
                         code_seed=w.code_seed, device=dev)
     wv = beta0.clone()
+    t_warm = time.perf_counter()
     if args.warmup is not None:
         warmup = args.warmup
         for t in range(warmup):
             sess.step(X, y, wv, mask(t), w.lr)
     else:
-        warmup, t0 = 0, time.perf_counter()
-        while warmup < 20 or time.perf_counter() - t0 < 0.25:
+        warmup = 0
+        while warmup < 20 or time.perf_counter() - t_warm < 0.25:
             for _ in range(20):
                 sess.step(X, y, wv, mask(warmup), w.lr)
                 warmup += 1
             torch.cuda.synchronize()
     torch.cuda.synchronize()
-    log("warm-up: %d steps (t = 0 fills the pipeline)" % warmup)
-    total = warmup + args.steps
+    warm_s = time.perf_counter() - t_warm
+    steps = args.steps
+    if steps is None:
+        # About one second of steps per pass (the warm-up's rate, which
+        # includes the slower t = 0 step, errs on the short side).
+        steps = int(min(1000, max(20, round(warmup / max(warm_s, 1e-9)))))
+    log("warm-up: %d steps (t = 0 fills the pipeline); timing %d passes of %d steps"
+        % (warmup, args.repeat, steps))
+    total = warmup + args.repeat * steps
 
     stream = torch.cuda.current_stream(dev)
     start = torch.cuda.Event(enable_timing=True)
@@ -262,23 +304,31 @@ def main():
                      else [P.PGC_KERNEL_GRADIENT])
     if args.all_kernel_times:
         timed_kernels = True
+    period = args.time_every
+    if period is None:
+        period = max(1, (args.repeat * steps) // TIMED_LAUNCH_TARGET)
     P.pgc_set_timing(sess.ctx, timed_kernels)
-    P.pgc_set_timing_period(sess.ctx, max(1, args.time_every))
-    torch.cuda.synchronize()
-    start.record(stream)
-    for t in range(warmup, total):
-        sess.step(X, y, wv, mask(t), w.lr)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    elapsed_ms = start.elapsed_time(stop)
+    P.pgc_set_timing_period(sess.ctx, max(1, period))
+    pass_ms = []
+    t = warmup
+    for _ in range(args.repeat):
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(steps):
+            sess.step(X, y, wv, mask(t), w.lr)
+            t += 1
+        stop.record(stream)
+        torch.cuda.synchronize()
+        pass_ms.append(start.elapsed_time(stop))
     kernels = {"gradient": P.PGC_KERNEL_GRADIENT, "reduce": P.PGC_KERNEL_REDUCE, "code": P.PGC_KERNEL_CODE,
                "mlp_cast": P.PGC_KERNEL_MLP_CAST, "mlp_forward": P.PGC_KERNEL_MLP_FORWARD,
                "mlp_head": P.PGC_KERNEL_MLP_HEAD, "mlp_wgrad": P.PGC_KERNEL_MLP_WGRAD}
-    per_launch = {}
-    for name, kid in kernels.items():
+    per_launch, timed_launches = {}, {}
+    for kname, kid in kernels.items():
         ms, launches = P.pgc_kernel_time(sess.ctx, kid)
         if launches:
-            per_launch[name] = ms / launches
+            per_launch[kname] = ms / launches
+            timed_launches[kname] = launches
     P.pgc_set_timing(sess.ctx, [])
     if not bool(torch.isfinite(wv).all()):
         print("non-finite weights after the timed steps", file=sys.stderr)
@@ -287,7 +337,7 @@ def main():
     # The warm-up step t = 0 (every worker evaluates all of its partitions),
     # timed on its own after starting the session over.  The same session
     # then repeats every step untimed, reading the decoded gradient out after
-    # each one; its final weights must equal the timed pass's bit for bit.
+    # each one; its final weights must equal the timed passes' bit for bit.
     sess.restart()
     w_check = beta0.clone()
     torch.cuda.synchronize()
@@ -297,15 +347,15 @@ def main():
     torch.cuda.synchronize()
     warmup_step_ms = start.elapsed_time(stop)
     steps_log = open(args.steps_log, "w") if args.steps_log else None
+    # Errors against the oracle only where its fp64 copy of X is small.
+    with_errors = steps_log is not None and w.N * w.d * 8 <= (2 << 30)
+    step_ms, recs = [warmup_step_ms], []
 
-    def log_step(t, step_ms):
-        survivors, _, scale = sess.decode_coeffs(mask(t))
-        steps_log.write(json.dumps({"t": t, "stragglers": [int(i) for i in mask(t).nonzero()[0]],
-                                    "survivors": [int(i) for i in survivors], "decode_scale": scale,
-                                    "step_ms": step_ms}) + "\n")
+    def keep(t):
+        if with_errors:
+            recs.append((sess.decoded().cpu().numpy(), w_check.cpu().numpy()))
 
-    if steps_log:
-        log_step(0, warmup_step_ms)
+    keep(0)
     for t in range(1, total):
         if steps_log:
             start.record(stream)
@@ -315,31 +365,48 @@ def main():
         sess.decoded()
         if steps_log:
             torch.cuda.synchronize()
-            log_step(t, start.elapsed_time(stop))
+            step_ms.append(start.elapsed_time(stop))
+            keep(t)
     torch.cuda.synchronize()
     if steps_log:
+        errors = oracle_errors(w, X, y, beta0, [mask(t) for t in range(total)], recs) if with_errors else None
+        for t in range(total):
+            survivors, _, scale = sess.decode_coeffs(mask(t))
+            rec = {"t": t, "stragglers": [int(i) for i in mask(t).nonzero()[0]],
+                   "survivors": [int(i) for i in survivors], "decode_scale": scale, "step_ms": step_ms[t]}
+            if errors:
+                rec["err_ghat"], rec["err_w"] = errors[t]
+            steps_log.write(json.dumps(rec) + "\n")
         steps_log.close()
+        if errors:
+            log("steps log: worst normwise error vs the oracle, ghat %.3g, w %.3g"
+                % (max(e[0] for e in errors), max(e[1] for e in errors)))
     reproduced = bool(torch.equal(w_check, wv))
     if not reproduced:
-        log("the repeated pass did not reproduce the timed pass's weights bit for bit")
+        log("the repeated pass did not reproduce the timed passes' weights bit for bit")
     del w_check
 
-    ms_per_step = elapsed_ms / args.steps
+    ms_per_step = sorted(pass_ms)[len(pass_ms) // 2] / steps
     steps_per_s = 1000.0 / ms_per_step
     grad_bytes, step_bytes = algorithmic_bytes(w)
+    step_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
     if w.model == "mlp":
         dominant = max(("mlp_forward", "mlp_wgrad"), key=lambda k: per_launch[k])
         achieved = mlp_gemm_flops(w) / (per_launch[dominant] * 1e-3) / 1e12
         roofline = {"bound": "mfma", "kernel": dominant, "achieved": achieved,
                     "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": read_traffic(w.name, "mfma")}
+                    "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": read_traffic(w.name, "mfma"),
+                    "timed_launches": timed_launches[dominant]}
     else:
         achieved = grad_bytes / (per_launch["gradient"] * 1e-3) / 1e9
         roofline = {"bound": "hbm", "kernel": "linear_gradient_kernel", "achieved": achieved,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                    "traffic": read_traffic(w.name, "hbm")}
-    log("step %.4f ms; per launch (ms): %s" % (ms_per_step, ", ".join(
-        "%s %.4f" % kv for kv in per_launch.items())))
+                    "traffic": read_traffic(w.name, "hbm"),
+                    "timed_launches": timed_launches["gradient"],
+                    "step_achieved": step_gbs, "step_frac": step_gbs / HBM_PEAK_GBS}
+    log("step %.4f ms (passes: %s ms); per launch (ms): %s" % (
+        ms_per_step, ", ".join("%.2f" % p for p in pass_ms),
+        ", ".join("%s %.4f" % kv for kv in per_launch.items())))
 
     baseline = None
     if args.cpu_seconds > 0:
@@ -352,7 +419,7 @@ def main():
         "value": steps_per_s,
         "unit": "steps/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": warmup,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
@@ -362,8 +429,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "scheme": w.scheme, "loss": w.model, "n": w.n, "c": w.c,
                    "N": w.N, "d": w.d, "q": w.q, "lr": w.lr, "seed": w.seed},
+        "repeat": args.repeat,
+        "pass_ms": pass_ms,
         "samples_per_s": {"unique_rows": rows * steps_per_s, "worker_samples": w.N * steps_per_s},
-        "step_hbm_gbs": step_bytes / (ms_per_step * 1e-3) / 1e9,
+        "step_hbm_gbs": step_gbs,
         "kernel_ms_per_launch": per_launch,
         "warmup_step_ms": warmup_step_ms,
         "timed_pass_reproduced": reproduced,

@@ -123,7 +123,11 @@ int pgc_configure(pgc_ctx* ctx, const pgc_config* cfg);
 int pgc_set_pipelining(pgc_ctx* ctx, int enabled);
 
 /* Stream (a hipStream_t, NULL = the null stream) on which pgc_step and the
- * pgc_read_* calls enqueue work.  Default: the null stream. */
+ * pgc_read_* calls enqueue work.  Default: the null stream.  When the stream
+ * changes, the call first synchronises the old stream, so the next step sees
+ * everything earlier steps wrote; if either stream is being captured into a
+ * graph it does not (that would end the capture) and the caller must order
+ * the two streams itself. */
 int pgc_set_stream(pgc_ctx* ctx, void* hip_stream);
 
 /* Bytes of device workspace the configured context needs (256-byte aligned). */

@@ -49,6 +49,10 @@ class PGCSession:
 
     def step(self, X, y, w, straggler_mask, lr):
         """One step; X, y, w are GPU tensors holding at least N*d_in, N and q elements."""
+        self._check_step_args(X, y, w)
+        _lib.pgc_step(self.ctx, X, y, w, straggler_mask, lr, self.n)
+
+    def _check_step_args(self, X, y, w):
         import torch
         x_dtype = torch.bfloat16 if self.model == "mlp" else torch.float32
         y_dtype = torch.int32 if self.model == "mlp" else torch.float32
@@ -57,7 +61,6 @@ class PGCSession:
             if t.dtype != dtype or t.numel() < numel or not t.is_contiguous() or t.device != self.device:
                 raise ValueError("%s must be a contiguous %s tensor of >= %d elements on %s"
                                  % (name, dtype, numel, self.device))
-        _lib.pgc_step(self.ctx, X, y, w, straggler_mask, lr, self.n)
 
     def restart(self):
         """Start over at t = 0 (the warm-up step) by binding the workspace again;

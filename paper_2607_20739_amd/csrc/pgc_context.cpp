@@ -12,6 +12,7 @@
 #include "pgc.h"
 #include "pgc_codes.h"
 #include "pgc_kernels.h"
+#include "pgc_step.h"
 
 namespace {
 
@@ -80,6 +81,7 @@ struct pgc_ctx {
   int64_t kpad = 0, m_pad = 0, pstride = 0;
   size_t off_ring = 0, off_coded = 0, off_decoded = 0, off_partials = 0, off_coef = 0, ws_need = 0;
   size_t off_w1t = 0, off_w2t = 0, off_w2p = 0, off_h = 0, off_dz1 = 0;
+  size_t partials_bytes = 0;  // linear models: block partial sums of the larger gradient grid
   char* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
@@ -151,7 +153,8 @@ void compute_layout(pgc_ctx* ctx) {
     const int64_t max_blocks =
         std::max<int64_t>(static_cast<int64_t>(ctx->warm.n_eval) * ctx->warm.blocks_per_part,
                           static_cast<int64_t>(ctx->pipe.n_eval) * ctx->pipe.blocks_per_part);
-    ctx->off_partials = take(sizeof(float) * static_cast<size_t>(max_blocks) * q);
+    ctx->partials_bytes = sizeof(float) * static_cast<size_t>(max_blocks) * q;
+    ctx->off_partials = take(ctx->partials_bytes);
   }
   ctx->ws_need = off;
 }
@@ -340,7 +343,25 @@ int pgc_set_pipelining(pgc_ctx* ctx, int enabled) {
 
 int pgc_set_stream(pgc_ctx* ctx, void* hip_stream) {
   if (ctx == nullptr) return PGC_EINVAL;
-  ctx->stream = static_cast<hipStream_t>(hip_stream);
+  hipStream_t next = static_cast<hipStream_t>(hip_stream);
+  if (next != ctx->stream) {
+    // Later steps read the ring, partials and w that steps enqueued on the old
+    // stream write: wait for them, unless either stream is being captured
+    // into a graph (a synchronisation there would end the capture; the
+    // caller orders the streams around a capture).
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(next, &cap);
+    if (e != hipSuccess) return device_fail(ctx, e, "hipStreamIsCapturing (new stream)");
+    if (cap == hipStreamCaptureStatusNone) {
+      e = hipStreamIsCapturing(ctx->stream, &cap);
+      if (e != hipSuccess) return device_fail(ctx, e, "hipStreamIsCapturing (old stream)");
+      if (cap == hipStreamCaptureStatusNone) {
+        e = hipStreamSynchronize(ctx->stream);
+        if (e != hipSuccess) return device_fail(ctx, e, "hipStreamSynchronize (old stream)");
+      }
+    }
+  }
+  ctx->stream = next;
   return PGC_OK;
 }
 
@@ -490,13 +511,14 @@ pgc::CodeArgs code_args(pgc_ctx* ctx, const pgc::Decode& dec, float* w, float lr
 // The linear models' step: the gradient kernel (a4), then one launch that
 // folds its partials into the ring (a5) and runs encode, decode and update (a6-a8).
 int linear_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::Decode& dec, float lr,
-                bool warm, int32_t part_stride, int32_t part_offset, int plane_first, int plane_count) {
+                bool warm, int32_t part_stride, int32_t part_offset, int plane_first, int plane_count,
+                float* partials) {
   const Grid& grid = warm ? ctx->warm : ctx->pipe;
   pgc::LinearGradArgs ga{};
   ga.X = static_cast<const float*>(X);
   ga.y = static_cast<const float*>(y);
   ga.w = w;
-  ga.partials = ws_ptr<float>(ctx, ctx->off_partials);
+  ga.partials = partials;
   ga.m = ctx->m;
   ga.rows_per_block = grid.rows_per_block;
   ga.d = static_cast<int32_t>(ctx->d);
@@ -635,10 +657,18 @@ int mlp_step(pgc_ctx* ctx, const void* X, const void* y, float* w, const pgc::De
 
 }  // namespace
 
-extern "C" {
+namespace pgc {
 
-int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
-             const uint8_t* straggler_mask, float lr) {
+size_t linear_partials_bytes(const pgc_ctx* ctx) { return ctx->partials_bytes; }
+
+bool context_is_linear(const pgc_ctx* ctx) { return ctx->configured && is_linear(ctx->cfg.model); }
+
+bool context_is_configured(const pgc_ctx* ctx) { return ctx->configured; }
+
+int set_error(pgc_ctx* ctx, int status, const char* msg) { return fail(ctx, status, msg); }
+
+int step_impl(pgc_ctx* ctx, const void* X, const void* y, float* w, const uint8_t* straggler_mask,
+              float lr, float* partials) {
   if (ctx == nullptr) return PGC_EINVAL;
   if (!ctx->configured) return fail(ctx, PGC_ESTATE, "pgc_configure first");
   if (ctx->ws == nullptr) return fail(ctx, PGC_ESTATE, "pgc_bind_workspace first");
@@ -680,11 +710,21 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
   roctxRangePushA(warm ? "pgc_step (warm-up)" : "pgc_step");
   const int st = ctx->cfg.model == PGC_MLP
                      ? mlp_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count)
-                     : linear_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count);
+                     : linear_step(ctx, X, y, w, dec, lr, warm, part_stride, part_offset, plane_first, plane_count,
+                                   partials ? partials : ws_ptr<float>(ctx, ctx->off_partials));
   roctxRangePop();
   if (st != PGC_OK) return st;
   ctx->t += 1;
   return PGC_OK;
+}
+
+}  // namespace pgc
+
+extern "C" {
+
+int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
+             const uint8_t* straggler_mask, float lr) {
+  return pgc::step_impl(ctx, X, y, w, straggler_mask, lr, nullptr);
 }
 
 namespace {

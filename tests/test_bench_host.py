@@ -28,9 +28,18 @@ def test_bench_measures_one_gpu_only():
 
 
 def test_bench_rejects_an_empty_timed_region():
-    res = run_bench("--steps", "0")
-    assert res.returncode == 2
-    assert "--steps" in res.stderr
+    for args in (("--steps", "0"), ("--repeat", "0"), ("--warmup", "0")):
+        res = run_bench(*args)
+        assert res.returncode == 2, args
+        assert "--steps" in res.stderr and "--repeat" in res.stderr
+
+
+def test_bench_defaults_to_the_largest_workload():
+    """With no --workload / --config the bench runs the 64 GiB PGC-CR workload."""
+    w = WORKLOADS[bench.DEFAULT_WORKLOAD]
+    assert bench.DEFAULT_WORKLOAD == ORDER[-1]
+    assert (w.scheme, w.model, w.n, w.c, w.d, w.N) == ("CR", "logistic", 128, 8, 8192, 2097152)
+    assert w.N * w.d * 4 == 64 << 30
 
 
 @pytest.mark.parametrize("name", [n for n in ORDER if WORKLOADS[n].model != "mlp"])

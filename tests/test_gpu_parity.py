@@ -6,9 +6,12 @@ gradient and the weights are compared after every step of independent
 trajectories (no re-syncing), normwise within 1e-5.
 
 Sizes: the small workloads run whole; the two large ones run their full
-trajectories with fewer rows per partition (same n, c, d, kernel shape) and,
-at full size, are checked on sampled partitions and by properties that hold
-at any size.
+trajectories with fewer rows per partition (same n, c, d, kernel shape).  At
+full size (the d = 1024, 4096 and 8192 workloads with all of their rows) every
+ring copy of sampled partitions written at each of c + 2 steps is compared
+with the oracle's gradient at the iterate that step started from (the oracle
+fed the GPU's iterate), and properties that hold at any size are checked:
+decode and update consistency, and bitwise reproducibility.
 """
 
 import numpy as np
@@ -408,13 +411,39 @@ def test_rejected_step_has_no_effect():
 FULL = ["crreal_lsq_n8_c3_d1024", "fr_logistic_n32_c4_d4096", "cr_logistic_n128_c8_d8192"]
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_full_size_ring_holds_partition_gradients(name):
+@pytest.fixture(scope="module", params=FULL)
+def full(request):
+    """Inputs of one full-size workload, generated once for every test that uses them."""
+    w = WORKLOADS[request.param]
+    _announce("%s full size: generating inputs" % w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    yield w, X, y, beta0
+    del X, y, beta0
+    torch.cuda.empty_cache()
+
+
+def _sampled_partitions(w):
+    return sorted({0, w.n // 2, w.n - 1})
+
+
+def _host_partition(w, X, y, k):
+    m = w.m
+    return (X[k * m:(k + 1) * m].double().cpu().numpy(), y[k * m:(k + 1) * m].double().cpu().numpy())
+
+
+def _fresh_holders(w, place, t, k):
+    """(worker, slot) pairs whose ring copy of partition k was written at step t."""
+    if t == 0:
+        return [(i, l) for i in range(w.n) for l in range(w.c) if place[i][l] == k]
+    o = (t - 1) % w.c
+    return [(i, o) for i in range(w.n) if place[i][o] == k]
+
+
+def test_full_size_ring_holds_partition_gradients(full):
     """With lr = 0 the weights stay at beta0, so every copy the ring ever holds
     is g_k(beta0); sampled partitions are compared with the oracle one by one."""
-    w = WORKLOADS[name]
-    _announce("%s full size, lr = 0" % name)
-    X, y, beta0 = make_inputs(w, device="cuda")
+    w, X, y, beta0 = full
+    _announce("%s full size, lr = 0" % w.name)
     sess = gpu_session(w)
     try:
         wv = beta0.clone()
@@ -422,12 +451,10 @@ def test_full_size_ring_holds_partition_gradients(name):
         for t in range(w.c + 1):
             sess.step(X, y, wv, masks[t], 0.0)
         place = sess.placement()
-        m = w.m
         beta_h = beta0.cpu().numpy().astype(np.float64)
-        for k in sorted({0, w.n // 2, w.n - 1}):
-            Xk = X[k * m:(k + 1) * m].cpu().numpy()
-            yk = y[k * m:(k + 1) * m].cpu().numpy()
-            g = O.partition_gradient(w.model, Xk.astype(np.float64), yk.astype(np.float64), beta_h)
+        for k in _sampled_partitions(w):
+            Xk, yk = _host_partition(w, X, y, k)
+            g = O.partition_gradient(w.model, Xk, yk, beta_h)
             holders = [(i, l) for i in range(w.n) for l in range(w.c) if place[i][l] == k]
             assert len(holders) == w.c
             for i, l in holders:
@@ -438,14 +465,52 @@ def test_full_size_ring_holds_partition_gradients(name):
         sess.close()
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_full_size_decode_and_update_are_consistent(name):
+def test_full_size_fresh_slots_match_the_oracle_at_every_iterate(full):
+    """At full size and the workload's learning rate, each step's freshly written
+    ring copies of sampled partitions equal the oracle's gradient of that
+    partition at the iterate the step started from (Sec. III gradient; the slot
+    the schedule of Sec. IV-A / V-B writes at step t), within the fp32 bar.
+    The oracle is fed the GPU's iterate (teacher-forced), so every step checks
+    the gradient kernel at a nonzero w over all of a partition's rows."""
+    w, X, y, beta0 = full
+    _announce("%s full size, teacher-forced slots over %d steps" % (w.name, w.c + 2))
+    sampled = _sampled_partitions(w)
+    host = {k: _host_partition(w, X, y, k) for k in sampled}
+    sess = gpu_session(w)
+    try:
+        place = sess.placement()
+        wv = beta0.clone()
+        checked = worst = 0.0
+        for t, mask in enumerate(gpu_masks(w, w.c + 2)):
+            w_before = wv.cpu().numpy().astype(np.float64)
+            sess.step(X, y, wv, mask, w.lr)
+            for k in sampled:
+                holders = _fresh_holders(w, place, t, k)
+                if not holders:
+                    continue
+                g = O.partition_gradient(w.model, host[k][0], host[k][1], w_before)
+                for i, l in holders:
+                    err = normwise_error(sess.ring(i, l).cpu().numpy(), g)
+                    worst = max(worst, err)
+                    checked += 1
+                    assert err <= FP32_TOL, "step %d, partition %d, worker %d slot %d: %.3g" % (
+                        t, k, i, l, err)
+            if t >= 1:
+                assert np.any(w_before != 0.0), "the iterate must have moved off w(0)"
+        # every sampled partition is checked at a pipelined step, not only at t = 0
+        for k in sampled:
+            assert any(_fresh_holders(w, place, t, k) for t in range(1, w.c + 2))
+        print("  %d slots checked, worst normwise error %.3g" % (checked, worst), flush=True)
+    finally:
+        sess.close()
+
+
+def test_full_size_decode_and_update_are_consistent(full):
     """At full size and the real learning rate: the decoded gradient is the
     weighted sum of the coded gradients with the library's decode weights, the
     coded gradients are the sums of the ring copies, and w moves by -lr * ghat."""
-    w = WORKLOADS[name]
-    _announce("%s full size, %d steps" % (name, w.c + 2))
-    X, y, beta0 = make_inputs(w, device="cuda")
+    w, X, y, beta0 = full
+    _announce("%s full size, %d steps" % (w.name, w.c + 2))
     sess = gpu_session(w)
     try:
         wv = beta0.clone()
@@ -469,3 +534,17 @@ def test_full_size_decode_and_update_are_consistent(name):
                 assert normwise_error(coded[j], ring) <= 1e-6
     finally:
         sess.close()
+
+
+def test_full_size_runs_are_bitwise_reproducible(full):
+    """Two runs of the same steps at full size (every kernel shape the workloads
+    use, including rows that span several waves) give bitwise the same decoded
+    gradient at every step and the same final weights."""
+    w, X, y, beta0 = full
+    _announce("%s full size, run twice" % w.name)
+    masks = gpu_masks(w, w.c + 2)
+    r1, w1 = gpu_run(w, X, y, beta0, masks, keep=("ghat",))
+    r2, w2 = gpu_run(w, X, y, beta0, masks, keep=("ghat",))
+    assert torch.equal(w1, w2)
+    for t, (a, b) in enumerate(zip(r1, r2)):
+        assert np.array_equal(a["ghat"], b["ghat"]), "step %d" % t
