@@ -18,7 +18,8 @@
  *   - "device pointer" = memory on the GPU the context runs on (e.g. a torch
  *     tensor's data_ptr()); "host pointer" = ordinary CPU memory.
  *   - The library never allocates GPU memory and never frees caller memory.
- *     All device scratch lives in a caller-provided workspace.
+ *     All device scratch lives in a caller-provided workspace, except the
+ *     fixed static array of pgc_step_noalloc.
  *   - A context is not thread-safe; use one context per stream.
  *   - Device work is enqueued on the context's stream and is not synchronised;
  *     device pointers must stay valid until the stream has passed the work.
@@ -161,6 +162,28 @@ int pgc_bind_workspace(pgc_ctx* ctx, void* dev_workspace, size_t bytes);
  * advance.  Returns without synchronising the stream. */
 int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
              const uint8_t* straggler_mask, float lr);
+
+/* Size of the fixed device array pgc_step_noalloc keeps its scratch in. */
+#define PGC_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * step as pgc_step, same arguments, checks, errors and results bit for bit,
+ * for the linear models (PGC_LOGISTIC, PGC_LSQ) only, with the gradient
+ * kernel's per-block partial sums in a library-owned static device array of
+ * PGC_NOALLOC_SCRATCH_BYTES bytes (one per GPU, held until the process ends)
+ * instead of the bound workspace.  The workspace still holds the ring, the
+ * coded and decoded gradients (its partial-sum region is not used).
+ * Calls no hipMalloc, hipFree or other allocating routine (with kernel timing
+ * off; pgc_set_timing creates its events on first use).
+ * Errors: PGC_EINVAL for the MLP, or when the configured shape's partial sums
+ * exceed PGC_NOALLOC_SCRATCH_BYTES (at most 1024 gradient blocks of d floats);
+ * PGC_EDEVICE if the array's device address cannot be found.  Every call on a
+ * GPU uses that GPU's one array: calls that overlap on one GPU (contexts on
+ * different streams) race and must be ordered by the caller.  The array keeps
+ * the last call's contents; every step overwrites what it reads. */
+int pgc_step_noalloc(pgc_ctx* ctx, const void* X, const void* y, float* w,
+                     const uint8_t* straggler_mask, float lr);
 
 /* Decode coefficients of `straggler_mask` (host, n bytes) for this context
  * (IS_SGD: d = 1 for every survivor, scale 1/|J|):

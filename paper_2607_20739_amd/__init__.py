@@ -62,6 +62,12 @@ class PGCSession:
                 raise ValueError("%s must be a contiguous %s tensor of >= %d elements on %s"
                                  % (name, dtype, numel, self.device))
 
+    def step_noalloc(self, X, y, w, straggler_mask, lr):
+        """The same step through pgc_step_noalloc (linear models; partial sums in
+        the library's fixed device array)."""
+        self._check_step_args(X, y, w)
+        _lib.pgc_step_noalloc(self.ctx, X, y, w, straggler_mask, lr, self.n)
+
     def restart(self):
         """Start over at t = 0 (the warm-up step) by binding the workspace again;
         the next step refills the whole ring."""

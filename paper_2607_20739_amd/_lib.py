@@ -20,6 +20,7 @@ PGC_POLICY_EXACT, PGC_POLICY_UNIFORM_COUNT, PGC_POLICY_BERNOULLI, PGC_POLICY_SLO
 PGC_KERNEL_GRADIENT, PGC_KERNEL_REDUCE, PGC_KERNEL_CODE = 0, 1, 2
 PGC_KERNEL_MLP_CAST, PGC_KERNEL_MLP_FORWARD, PGC_KERNEL_MLP_HEAD, PGC_KERNEL_MLP_WGRAD = 3, 4, 5, 6
 PGC_MAX_N = 256
+PGC_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 SCHEMES = {"FR": PGC_FR, "CR": PGC_CR, "CR_REAL": PGC_CR_REAL, "IS_SGD": PGC_IS_SGD}
 MODELS = {"logistic": PGC_LOGISTIC, "lsq": PGC_LSQ, "mlp": PGC_MLP}
@@ -51,6 +52,7 @@ _SIGNATURES = {
     "pgc_workspace_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "pgc_bind_workspace": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
     "pgc_step": (ctypes.c_int, [_P, _P, _P, _P, _U8P, ctypes.c_float]),
+    "pgc_step_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _U8P, ctypes.c_float]),
     "pgc_decode_coeffs": (ctypes.c_int, [_P, _U8P, _F64P, _F64P, _I32P, _I32P]),
     "pgc_placement": (ctypes.c_int, [_P, _I32P]),
     "pgc_schedule": (ctypes.c_int, [_P, ctypes.c_int64, _I32P]),
@@ -166,6 +168,14 @@ def pgc_step(ctx, X, y, w, straggler_mask, lr, n):
     _, mp = _mask_arg(straggler_mask, n)
     _check(lib().pgc_step(ctx, _P(_dev(X)), _P(_dev(y)), _P(_dev(w, torch.float32)), mp,
                           ctypes.c_float(lr)), ctx)
+
+
+def pgc_step_noalloc(ctx, X, y, w, straggler_mask, lr, n):
+    """pgc_step with the partial sums in the library's fixed device array."""
+    import torch
+    _, mp = _mask_arg(straggler_mask, n)
+    _check(lib().pgc_step_noalloc(ctx, _P(_dev(X)), _P(_dev(y)), _P(_dev(w, torch.float32)), mp,
+                                  ctypes.c_float(lr)), ctx)
 
 
 def pgc_decode_coeffs(ctx, straggler_mask, n):
