@@ -173,27 +173,6 @@ def copy_calibration(nbytes):
     return 0
 
 
-def oracle_errors(w, X, y, beta0, masks, recs):
-    """Per-step normwise errors of the decoded gradient and the weights of the
-    repeat pass against the oracle run on the same inputs and masks (CPU)."""
-    import numpy as np
-    from oracle import pgc_oracle as O
-    from oracle import rng as R
-    schemes = {"FR": O.FR, "CR": O.CR, "CR_REAL": O.CR_REAL}
-    B = None
-    if w.scheme == "CR_REAL":
-        B = O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
-    shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
-    ref = O.run(schemes[w.scheme], w.model, w.n, w.c, X.float().cpu().numpy(), y.cpu().numpy(),
-                beta0.cpu().numpy(), w.lr, masks, B=B, shape=shape, keep_coded=False, keep_alpha=False)
-
-    def err(a, b):
-        scale = np.max(np.abs(b))
-        diff = np.max(np.abs(np.asarray(a, np.float64) - b))
-        return float(diff / scale) if scale > 0 else float(diff)
-    return [(err(g, o.ghat), err(wv, o.beta)) for (g, wv), o in zip(recs, ref)]
-
-
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,8 +190,9 @@ def main():
     ap.add_argument("--seed", type=int, default=None, help="override the workload's data and mask seed")
     ap.add_argument("--steps-log", default="", metavar="PATH",
                     help="write one JSON line per step of the untimed repeat pass (t, stragglers, "
-                         "survivors, decode scale, step time, and on workloads whose fp64 copy fits "
-                         "in 2 GiB the normwise errors of ghat and w against the oracle)")
+                         "survivors, decode scale, step time) and, when they take at most 512 MiB, "
+                         "every step's decoded gradient and weights to PATH.npz (tests/"
+                         "steps_log_errors.py adds the per-step errors against the oracle)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--all-kernel-times", action="store_true",
@@ -347,13 +327,14 @@ def main():
     torch.cuda.synchronize()
     warmup_step_ms = start.elapsed_time(stop)
     steps_log = open(args.steps_log, "w") if args.steps_log else None
-    # Errors against the oracle only where its fp64 copy of X is small.
-    with_errors = steps_log is not None and w.N * w.d * 8 <= (2 << 30)
-    step_ms, recs = [warmup_step_ms], []
+    # Every step's decoded gradient and weights, where they fit in 512 MiB.
+    keep_vectors = steps_log is not None and 2 * total * w.q * 4 <= (512 << 20)
+    step_ms, ghats, ws = [warmup_step_ms], [], []
 
     def keep(t):
-        if with_errors:
-            recs.append((sess.decoded().cpu().numpy(), w_check.cpu().numpy()))
+        if keep_vectors:
+            ghats.append(sess.decoded().cpu())
+            ws.append(w_check.cpu())
 
     keep(0)
     for t in range(1, total):
@@ -369,18 +350,16 @@ def main():
             keep(t)
     torch.cuda.synchronize()
     if steps_log:
-        errors = oracle_errors(w, X, y, beta0, [mask(t) for t in range(total)], recs) if with_errors else None
         for t in range(total):
             survivors, _, scale = sess.decode_coeffs(mask(t))
             rec = {"t": t, "stragglers": [int(i) for i in mask(t).nonzero()[0]],
                    "survivors": [int(i) for i in survivors], "decode_scale": scale, "step_ms": step_ms[t]}
-            if errors:
-                rec["err_ghat"], rec["err_w"] = errors[t]
             steps_log.write(json.dumps(rec) + "\n")
         steps_log.close()
-        if errors:
-            log("steps log: worst normwise error vs the oracle, ghat %.3g, w %.3g"
-                % (max(e[0] for e in errors), max(e[1] for e in errors)))
+        if keep_vectors:
+            import numpy as np
+            np.savez(args.steps_log + ".npz", ghat=torch.stack(ghats).numpy(), w=torch.stack(ws).numpy(),
+                     workload=w.name, lr=w.lr, seed=w.seed)
     reproduced = bool(torch.equal(w_check, wv))
     if not reproduced:
         log("the repeated pass did not reproduce the timed passes' weights bit for bit")

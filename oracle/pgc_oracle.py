@@ -339,6 +339,58 @@ class StepRecord:
     losses: dict = field(default_factory=dict)
 
 
+def decode_step(scheme, n, c, E, grad, t, mask, shape, B=None, pipelined=True):
+    """Coded gradients and decoded gradient of step t.
+
+    grad(k, tau) is the gradient of partition k at the iterate of step tau;
+    E the encoding coefficients.  Each worker's coded gradient combines the
+    copies coded_terms lists (Sec. IV-A, V-A, V-B); the master decodes the
+    survivors' words with decode_weights.  Returns (coded, staleness,
+    survivors, d, scale, ghat).
+    """
+    coded = []
+    stale = []
+    for i in range(n):
+        terms = coded_terms(scheme, n, c, i, t, pipelined)
+        word = np.zeros(shape)
+        for slot, k, tau in terms:
+            word = word + E[i][slot] * grad(k, tau)
+        coded.append(word)
+        stale.append([(k, tau) for slot, k, tau in terms])
+    J = survivors(mask)
+    d, scale = decode_weights(scheme, n, c, J, B)
+    acc = np.zeros(shape)
+    for dm, j in zip(d, J):
+        acc = acc + dm * coded[j]
+    return coded, stale, J, d, scale, scale * acc
+
+
+def teacher_forced_ghat(scheme, model, n, c, X, y, iterates, t, mask, B=None, shape=None,
+                        pipelined=True, memo=None):
+    """Decoded gradient of step t with every copy evaluated at given iterates.
+
+    iterates[tau] is the parameter vector the step tau started from (taken
+    from the run being diagnosed, not from the oracle's own trajectory), so a
+    per-step difference separates the error of one step from the drift of two
+    independent trajectories.  Same definitions as run().  `memo` (a dict)
+    may carry partition gradients from one call to the next when the earlier
+    iterates are unchanged.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    y = np.asarray(y, dtype=np.float64)
+    m = X.shape[0] // n
+    E = encoding_coefficients(scheme, n, c, B)
+    memo = {} if memo is None else memo
+
+    def grad(k, tau):
+        if (k, tau) not in memo:
+            rows = slice(k * m, (k + 1) * m)
+            memo[(k, tau)] = partition_gradient(model, X[rows], y[rows],
+                                                np.asarray(iterates[tau], dtype=np.float64), shape)
+        return memo[(k, tau)]
+    return decode_step(scheme, n, c, E, grad, t, mask, np.shape(iterates[t]), B=B, pipelined=pipelined)[-1]
+
+
 def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
         keep_coded=True, keep_alpha=True, pipelined=True):
     """Run len(masks) PGC steps t = 0, 1, ... from beta0 and return one StepRecord per step.
@@ -368,21 +420,8 @@ def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
 
     records = []
     for t, mask in enumerate(masks):
-        coded = []
-        stale = []
-        for i in range(n):
-            terms = coded_terms(scheme, n, c, i, t, pipelined)
-            word = np.zeros_like(history[t])
-            for slot, k, tau in terms:
-                word = word + E[i][slot] * grad(k, tau)
-            coded.append(word)
-            stale.append([(k, tau) for slot, k, tau in terms])
-        J = survivors(mask)
-        d, scale = decode_weights(scheme, n, c, J, B)
-        acc = np.zeros_like(history[t])
-        for dm, j in zip(d, J):
-            acc = acc + dm * coded[j]
-        ghat = scale * acc
+        coded, stale, J, d, scale, ghat = decode_step(scheme, n, c, E, grad, t, mask, history[t].shape,
+                                                      B=B, pipelined=pipelined)
         beta_next = history[t] - lr * ghat
         history[t + 1] = beta_next
         evaluated = ([P[i][l] for i in range(n) for l in range(c)] if (t == 0 or not pipelined)

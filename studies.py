@@ -222,17 +222,29 @@ def window_extremes(values, every, pick):
     return [round(pick(values[i:i + every]), 3) for i in range(0, len(values), every)]
 
 
+NAIVE_CR_N, NAIVE_CR_S = 12, 5
+NAIVE_CR_MASK_SEED = (12 << 32) | 1
+
+
+def naive_cr_workload(rows_per_partition, d, lr, steps):
+    """Data of the naive-CR study: n = 12 workers, c = 6, logistic labels."""
+    n, s = NAIVE_CR_N, NAIVE_CR_S
+    return Workload("study_naive_cr", "CR_REAL", "logistic", n=n, c=s + 1, N=n * rows_per_partition, d=d,
+                    lr=lr, steps=steps, policy=POLICY_EXACT, cap=s, seed=12, code_seed=12)
+
+
 def study_naive_cr(args, out):
     import numpy as np
     import torch
-    n, s = 12, 5
+    n, s = NAIVE_CR_N, NAIVE_CR_S
     dev = torch.device("cuda", 0)
-    data = Workload("study_naive_cr", "CR_REAL", "logistic", n=n, c=s + 1, N=n * args.rows_per_partition,
-                    d=args.d, lr=args.lr, steps=args.steps, policy=POLICY_EXACT, cap=s, seed=12, code_seed=12)
-    X, y, beta0 = make_inputs(data, device=dev)
+    data = naive_cr_workload(args.rows_per_partition, args.d, args.lr, args.steps)
+    # Drawn on the host, so the fp64 control (tests/naive_cr_oracle.py) can
+    # draw the very same data without a GPU.
+    X, y, beta0 = (t.to(dev) for t in make_inputs(data, device="cpu"))
     results = {}
     for name in ["PGC-FR", "PGC-CR", "naive PGC-CR"]:
-        masks, _ = delay_masks(n, s, args.steps, (12 << 32) | 1, 1.0, 1.0, name, s)
+        masks, _ = delay_masks(n, s, args.steps, NAIVE_CR_MASK_SEED, 1.0, 1.0, name, s)
         losses, alphas = train(name, s, data, X, y, beta0, masks, args.lr, record_alpha=True)
         amax = [a for a, _ in alphas]
         amin = [b for _, b in alphas]
