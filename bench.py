@@ -177,7 +177,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed steps per pass (default: about 1 s of steps, between 20 and 1000)")
+                    help="timed steps per pass (default: about 1 s of steps, between 20 and 100,000)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps before the timed ones (default: at least 20 and at least "
                          "0.25 s of steps, so the GPU's clocks have ramped up)")
@@ -271,7 +271,7 @@ def main():
     if steps is None:
         # About one second of steps per pass (the warm-up's rate, which
         # includes the slower t = 0 step, errs on the short side).
-        steps = int(min(1000, max(20, round(warmup / max(warm_s, 1e-9)))))
+        steps = int(min(100000, max(20, round(warmup / max(warm_s, 1e-9)))))
     log("warm-up: %d steps (t = 0 fills the pipeline); timing %d passes of %d steps"
         % (warmup, args.repeat, steps))
     total = warmup + args.repeat * steps

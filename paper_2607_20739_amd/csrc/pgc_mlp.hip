@@ -71,15 +71,14 @@ void mlp_cast_w2_kernel(MlpCastArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// forward: H = relu(X W1 + b1).  Block tile 256 rows x 256 hidden, K step 32,
+// forward: H = relu(X W1 + b1).  Block tile 256 rows x 256 hidden, K step 64,
 // 8 waves as 2 (rows) x 4 (hidden), 128 x 64 each, one block per CU.  Tiles
 // travel from global memory straight into LDS (16 bytes per lane, no register
-// staging) through four buffers, three K steps ahead: one barrier per K step.
-// In a tile row of 32 bf16 (four 16-byte chunks) chunk ch of row r sits at
-// slot ch ^ (((r >> 1) ^ (r >> 2)) & 3): any 8 consecutive rows of a 16-row
-// fragment read fall on distinct 16-byte slots modulo 128 bytes, and all 16
-// modulo 256 bytes.  The MFMAs produce H^T (A = W1^T rows, B = X rows), which leaves four
-// consecutive hidden units of one sample in each lane: one 8-byte store.
+// staging) through two buffers, loaded one K step ahead: one barrier per K
+// step.  In a tile row of 64 bf16 (eight 16-byte chunks) chunk ch of row r
+// sits at slot ch ^ ((r ^ (r >> 3)) & 7), so the 16 rows of a fragment read
+// spread over the slots.  The MFMAs produce H^T (A = W1^T rows, B = X rows),
+// which leaves four consecutive hidden units of one sample in each lane.
 // Block ids are mapped so that all hidden tiles of a row tile run on the same
 // XCD (workgroups are dealt to the 8 XCDs round-robin) and share its L2.
 // ---------------------------------------------------------------------------
@@ -209,7 +208,8 @@ void mlp_forward_kernel(MlpForwardArgs a) {
     if (p < ksteps) issue(p, p);
   for (int ks = 0; ks < ksteps; ++ks) {
     // This wave's loads of step ks have landed; after the barrier every
-    // wave's have, and every wave is done reading buffer (ks - 1) % 4.
+    // wave's have, and every wave is done reading buffer (ks - 1) % kFwStages,
+    // which the loads of step ks + kFwStages - 1 then overwrite.
     const int later = min(kFwStages - 2, ksteps - 1 - ks);
     if (later >= 2) wait_vmcnt<(kFwStages >= 4 ? 2 * kLoads : 0)>();
     else if (later == 1) wait_vmcnt<(kFwStages >= 3 ? kLoads : 0)>();

@@ -149,12 +149,22 @@ def test_mlp_resume_from_saved_state_is_bitwise_identical():
         b.close()
 
 
-def test_full_size_mlp_ring_holds_partition_gradients():
+@pytest.fixture(scope="module")
+def full_mlp():
+    """Inputs of the full 784 -> 1024 -> 10 workload (N = 1048576), drawn once."""
+    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+    _announce("%s full size: generating inputs" % w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    yield w, X, y, beta0
+    del X, y, beta0
+    torch.cuda.empty_cache()
+
+
+def test_full_size_mlp_ring_holds_partition_gradients(full_mlp):
     """Full size (N = 1048576), lr = 0: sampled partitions' ring copies equal the
     oracle's gradient at beta0, computed one partition at a time."""
-    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+    w, X, y, beta0 = full_mlp
     _announce("%s full size, lr = 0" % w.name)
-    X, y, beta0 = make_inputs(w, device="cuda")
     sess = gpu_session(w)
     try:
         wv = beta0.clone()
@@ -175,10 +185,54 @@ def test_full_size_mlp_ring_holds_partition_gradients():
         sess.close()
 
 
-def test_full_size_mlp_decode_and_update_are_consistent():
-    w = WORKLOADS["cr_mlp_n64_c4_784x1024x10"]
+def test_full_size_mlp_fresh_slots_match_the_oracle_at_every_iterate(full_mlp):
+    """Full size at the workload's learning rate: each step's freshly written
+    ring copies of sampled partitions equal the oracle's gradient of that
+    partition (all 16,384 rows) at the iterate the step started from (the
+    oracle fed the GPU's iterate), within the bf16 bar, for c + 2 steps."""
+    w, X, y, beta0 = full_mlp
+    _announce("%s full size, teacher-forced slots over %d steps" % (w.name, w.c + 2))
+    shape = (w.d, w.hidden, w.classes)
+    sampled = (0, w.n // 2, w.n - 1)
+    host = {k: (X[k * w.m:(k + 1) * w.m].float().cpu().numpy().astype(np.float64),
+                y[k * w.m:(k + 1) * w.m].cpu().numpy()) for k in sampled}
+    sess = gpu_session(w)
+    try:
+        place = sess.placement()
+        wv = beta0.clone()
+        worst, checked = 0.0, 0
+        for t, mask in enumerate(gpu_masks(w, w.c + 2)):
+            w_before = wv.cpu().numpy().astype(np.float64)
+            sess.step(X, y, wv, mask, w.lr)
+            o = (t - 1) % w.c
+            for k in sampled:
+                holders = ([(i, l) for i in range(w.n) for l in range(w.c) if place[i][l] == k] if t == 0
+                           else [(i, o) for i in range(w.n) if place[i][o] == k])
+                g = O.partition_gradient(O.MLP, host[k][0], host[k][1], w_before, shape)
+                for i, l in holders:
+                    err = normwise_error(sess.ring(i, l).cpu().numpy(), g)
+                    worst = max(worst, err)
+                    checked += 1
+                    assert err <= BF16_TOL, "step %d, partition %d, worker %d slot %d: %.3g" % (t, k, i, l, err)
+        print("  %d slots checked, worst normwise error %.3g" % (checked, worst), flush=True)
+    finally:
+        sess.close()
+
+
+def test_full_size_mlp_runs_are_bitwise_reproducible(full_mlp):
+    w, X, y, beta0 = full_mlp
+    _announce("%s full size, run twice" % w.name)
+    masks = gpu_masks(w, 3)
+    r1, w1 = gpu_run(w, X, y, beta0, masks, keep=("ghat",))
+    r2, w2 = gpu_run(w, X, y, beta0, masks, keep=("ghat",))
+    assert torch.equal(w1, w2)
+    for t, (a, b) in enumerate(zip(r1, r2)):
+        assert np.array_equal(a["ghat"], b["ghat"]), "step %d" % t
+
+
+def test_full_size_mlp_decode_and_update_are_consistent(full_mlp):
+    w, X, y, beta0 = full_mlp
     _announce("%s full size, %d steps" % (w.name, 3))
-    X, y, beta0 = make_inputs(w, device="cuda")
     sess = gpu_session(w)
     try:
         wv = beta0.clone()
