@@ -176,6 +176,9 @@ int pgc_step(pgc_ctx* ctx, const void* X, const void* y, float* w,
  * coded and decoded gradients (its partial-sum region is not used).
  * Calls no hipMalloc, hipFree or other allocating routine (with kernel timing
  * off; pgc_set_timing creates its events on first use).
+ * The array used is the one of the current device, which must be the GPU of
+ * the context's stream (as for any launch on that stream); its address is
+ * looked up on the first call on each device.
  * Errors: PGC_EINVAL for the MLP, or when the configured shape's partial sums
  * exceed PGC_NOALLOC_SCRATCH_BYTES (at most 1024 gradient blocks of d floats);
  * PGC_EDEVICE if the array's device address cannot be found.  Every call on a

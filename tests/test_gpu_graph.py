@@ -108,3 +108,37 @@ def test_side_stream_matches_default_stream():
     torch.cuda.current_stream().wait_stream(side)
     b.close()
     assert torch.equal(wa, wb)
+
+
+def test_switching_streams_mid_run_keeps_the_step_order():
+    """Steps queued on one stream, then more steps after pgc_set_stream moves the
+    session to another stream with no wait by the caller: the library orders
+    the two streams itself, so the weights equal a single-stream run's bit for
+    bit."""
+    from workloads import WORKLOADS
+    w = WORKLOADS["crreal_lsq_n8_c3_d1024"].resized(N=8 * 8192, steps=30)
+    _announce("stream switch " + w.name)
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks = [P.pgc_make_mask(w.mask_seed, t, w.policy, w.n, w.cap, w.p) for t in range(w.steps)]
+    ref = _session(w)
+    wr = beta0.clone()
+    for m in masks:
+        ref.step(X, y, wr, m, w.lr)
+    torch.cuda.synchronize()
+    ref.close()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()     # default priority
+    s1.wait_stream(torch.cuda.current_stream())
+    sess = _session(w)
+    ws = beta0.clone()
+    try:
+        sess.set_stream(s1)
+        for m in masks[:20]:            # ~20 queued steps, nothing waited for
+            sess.step(X, y, ws, m, w.lr)
+        sess.set_stream(s2)
+        for m in masks[20:]:
+            sess.step(X, y, ws, m, w.lr)
+        s2.synchronize()
+        torch.cuda.current_stream().wait_stream(s2)
+        assert torch.equal(ws, wr)
+    finally:
+        sess.close()
