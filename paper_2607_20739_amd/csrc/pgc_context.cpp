@@ -665,6 +665,8 @@ bool context_is_linear(const pgc_ctx* ctx) { return ctx->configured && is_linear
 
 bool context_is_configured(const pgc_ctx* ctx) { return ctx->configured; }
 
+bool context_has_workspace(const pgc_ctx* ctx) { return ctx->ws != nullptr; }
+
 int set_error(pgc_ctx* ctx, int status, const char* msg) { return fail(ctx, status, msg); }
 
 int step_impl(pgc_ctx* ctx, const void* X, const void* y, float* w, const uint8_t* straggler_mask,

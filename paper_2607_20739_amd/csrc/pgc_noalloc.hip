@@ -54,6 +54,7 @@ extern "C" int pgc_step_noalloc(pgc_ctx* ctx, const void* X, const void* y, floa
                             std::to_string(static_cast<size_t>(PGC_NOALLOC_SCRATCH_BYTES)) + " bytes";
     return pgc::set_error(ctx, PGC_EINVAL, msg.c_str());
   }
+  if (!pgc::context_has_workspace(ctx)) return pgc::set_error(ctx, PGC_ESTATE, "pgc_bind_workspace first");
   float* partials = nullptr;
   const hipError_t e = scratch_ptr(&partials);
   if (e != hipSuccess) {

@@ -20,6 +20,7 @@ int step_impl(pgc_ctx* ctx, const void* X, const void* y, float* w, const uint8_
 size_t linear_partials_bytes(const pgc_ctx* ctx);
 
 bool context_is_configured(const pgc_ctx* ctx);
+bool context_has_workspace(const pgc_ctx* ctx);
 bool context_is_linear(const pgc_ctx* ctx);
 
 // Records `msg` as the context's last error and returns `status`.

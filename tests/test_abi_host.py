@@ -231,3 +231,90 @@ def test_state_size_is_the_header_and_the_ring():
         assert e.value.status == P.PGC_ESTATE
     finally:
         P.pgc_destroy(ctx)
+
+
+def test_noalloc_step_rejects_on_the_host_before_any_device_work():
+    """pgc_step_noalloc's argument checks run before it touches a GPU: an
+    unconfigured context, the MLP, a shape whose block partial sums exceed the
+    fixed array, and a missing workspace are all rejected on the host."""
+    mask = np.zeros(4, np.uint8)
+    ctx = P.pgc_init("CR", 4, 2, 64)
+    try:
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_step_noalloc(ctx, 1, 1, 1, mask, 0.1, 4)
+        assert e.value.status == P.PGC_ESTATE
+        P.pgc_configure(ctx, "lsq", 4 * 4096, 64)
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_step_noalloc(ctx, 1, 1, 1, mask, 0.1, 4)    # fits, but nothing is bound
+        assert e.value.status == P.PGC_ESTATE and "workspace" in P.pgc_last_error(ctx)
+    finally:
+        P.pgc_destroy(ctx)
+    q = 64 * 256 + 256 + 256 * 10 + 10
+    ctx = P.pgc_init("CR", 4, 2, q)
+    try:
+        P.pgc_configure(ctx, "mlp", 4 * 64, 64, 256, 10)
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_step_noalloc(ctx, 1, 1, 1, mask, 0.1, 4)
+        assert e.value.status == P.PGC_EINVAL and "linear" in P.pgc_last_error(ctx)
+    finally:
+        P.pgc_destroy(ctx)
+    # d = 32768 on 512 gradient blocks of 128 KiB of partial sums each: 64 MiB, over the limit.
+    ctx = P.pgc_init("CR", 4, 2, 32768)
+    try:
+        P.pgc_configure(ctx, "lsq", 4 * 2048, 32768)
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_step_noalloc(ctx, 1, 1, 1, mask, 0.1, 4)
+        assert e.value.status == P.PGC_EINVAL and "scratch" in P.pgc_last_error(ctx)
+        assert P.pgc_get_step(ctx) == 0
+    finally:
+        P.pgc_destroy(ctx)
+
+
+def _random_admissible_case(data):
+    from hypothesis import strategies as st
+    scheme = data.draw(st.sampled_from(["FR", "CR", "CR_REAL", "IS_SGD"]), label="scheme")
+    if scheme == "FR":
+        c = data.draw(st.integers(1, 8), label="c")
+        n = c * data.draw(st.integers(1, 256 // c), label="groups")
+    elif scheme == "CR":
+        n = data.draw(st.integers(1, 256), label="n")
+        c = data.draw(st.integers(1, min(n, 8)), label="c")
+    elif scheme == "CR_REAL":
+        n = data.draw(st.integers(2, 16), label="n")
+        c = data.draw(st.integers(1, min(n, 4)), label="c")
+    else:
+        n, c = data.draw(st.integers(1, 256), label="n"), 1
+    cap = n - 1 if scheme == "IS_SGD" else c - 1
+    k = data.draw(st.integers(0, cap), label="stragglers")
+    strag = data.draw(st.lists(st.integers(0, n - 1), min_size=k, max_size=k, unique=True), label="who")
+    mask = np.zeros(n, np.uint8)
+    mask[strag] = 1
+    return scheme, n, c, mask
+
+
+def test_decode_coefficients_match_the_oracle_on_random_cases():
+    """Random schemes, sizes up to n = 256 and admissible straggler sets: the
+    library's survivors, decode weights and scale equal the oracle's (bit for
+    bit except the real code's least-squares weights)."""
+    from hypothesis import given, settings, strategies as st
+
+    @settings(max_examples=300, deadline=None, derandomize=True)
+    @given(st.data())
+    def check(data):
+        scheme, n, c, mask = _random_admissible_case(data)
+        ctx = _ctx(scheme, n, c, code_seed=11)
+        try:
+            B_or = (O.cyclic_encoding_matrix(n, c, R.null_space_generator(11, c - 1, n))
+                    if scheme == "CR_REAL" else None)
+            surv, d, scale = P.pgc_decode_coeffs(ctx, mask, n)
+            J = O.survivors(mask)
+            d_or, scale_or = O.decode_weights(SCHEME_NAMES[scheme], n, c, J, B_or)
+            assert surv.tolist() == J
+            if scheme == "CR_REAL":
+                assert scale == pytest.approx(scale_or, rel=1e-15)
+                np.testing.assert_allclose(d, d_or, rtol=1e-9, atol=1e-9 * max(1.0, np.abs(d_or).max()))
+            else:
+                assert scale == scale_or and d.tolist() == d_or.tolist()
+        finally:
+            P.pgc_destroy(ctx)
+    check()
