@@ -275,6 +275,7 @@ def main():
     log("warm-up: %d steps (t = 0 fills the pipeline); timing %d passes of %d steps"
         % (warmup, args.repeat, steps))
     total = warmup + args.repeat * steps
+    mask(total - 1)   # every step's straggler mask, drawn before the timed passes
 
     stream = torch.cuda.current_stream(dev)
     start = torch.cuda.Event(enable_timing=True)
