@@ -392,13 +392,15 @@ def teacher_forced_ghat(scheme, model, n, c, X, y, iterates, t, mask, B=None, sh
 
 
 def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
-        keep_coded=True, keep_alpha=True, pipelined=True):
+        keep_coded=True, keep_alpha=True, pipelined=True, on_step=None):
     """Run len(masks) PGC steps t = 0, 1, ... from beta0 and return one StepRecord per step.
 
     masks[t] is the straggler mask of step t (1 = straggles).  Step 0 is the
     warm-up: every worker evaluates all c of its partitions at beta0
     (Sec. IV-A), so its coded gradient is the gradient-coding word.
     pipelined=False runs gradient coding: every step is such a step.
+    on_step(t, record), when given, is called after each step (progress
+    reports of long runs); it does not affect the run.
     """
     X = np.asarray(X, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
@@ -432,6 +434,8 @@ def run(scheme, model, n, c, X, y, beta0, lr, masks, B=None, shape=None,
             coded=np.array(coded) if keep_coded else None,
             copy_counts=copy_counts(scheme, n, c, J),
             alpha=decoding_coefficients(scheme, n, c, J, d, B) if keep_alpha else None))
+        if on_step is not None:
+            on_step(t, records[-1])
         # Step t + 1 combines copies from steps >= t + 2 - c only (with step 0
         # standing in for the steps before the pipeline filled).
         oldest = t + 2 - c

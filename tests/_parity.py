@@ -42,11 +42,17 @@ def oracle_code_matrix(w):
     return O.cyclic_encoding_matrix(w.n, w.c, R.null_space_generator(w.code_seed, w.c - 1, w.n))
 
 
-def oracle_run(w, X, y, beta0, masks, lr=None, keep_coded=False, pipelined=True):
+def oracle_run(w, X, y, beta0, masks, lr=None, keep_coded=False, pipelined=True, progress_every=0):
+    """The oracle's trajectory; with progress_every > 0 it prints a line every
+    that many steps (long full-size runs)."""
     shape = (w.d, w.hidden, w.classes) if w.model == "mlp" else None
+
+    def report(t, rec):
+        if progress_every and (t + 1) % progress_every == 0:
+            print("  oracle: %d of %d steps done" % (t + 1, len(masks)), flush=True)
     return O.run(SCHEMES[w.scheme], w.model, w.n, w.c, X, y, beta0, w.lr if lr is None else lr,
                  masks, B=oracle_code_matrix(w), shape=shape, keep_coded=keep_coded,
-                 keep_alpha=False, pipelined=pipelined)
+                 keep_alpha=False, pipelined=pipelined, on_step=report)
 
 
 def gpu_session(w, device="cuda", pipelined=True):

@@ -43,7 +43,7 @@ def _to_host(*tensors):
     return [t.cpu().numpy() for t in tensors]
 
 
-def _check_trajectory(w, X, y, beta0, steps=None, X_host=None, pipelined=True):
+def _check_trajectory(w, X, y, beta0, steps=None, X_host=None, pipelined=True, progress_every=0):
     masks_gpu = gpu_masks(w, steps)
     masks_or = oracle_masks(w, steps)
     for t, (a, b) in enumerate(zip(masks_gpu, masks_or)):
@@ -51,7 +51,7 @@ def _check_trajectory(w, X, y, beta0, steps=None, X_host=None, pipelined=True):
     recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu, pipelined=pipelined)
     Xh = X_host if X_host is not None else X.cpu().numpy()
     yh, bh = _to_host(y, beta0)
-    recs_or = oracle_run(w, Xh, yh, bh, masks_or, pipelined=pipelined)
+    recs_or = oracle_run(w, Xh, yh, bh, masks_or, pipelined=pipelined, progress_every=progress_every)
     worst = worst_elem = 0.0
     for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
         e_g = normwise_error(g["ghat"], o.ghat)
@@ -85,6 +85,18 @@ def test_workload_trajectory_matches_oracle(name, resize):
     _announce("%s N=%d d=%d steps=%d" % (w.name, w.N, w.d, w.steps))
     X, y, beta0 = make_inputs(w, device="cuda")
     _check_trajectory(w, X, y, beta0)
+
+
+def test_full_size_fr_d4096_trajectory_matches_oracle():
+    """The FR workload with all 1,048,576 rows (16 GiB of features): the GPU's
+    decoded gradient and weights after every one of its 50 steps against the
+    oracle's independent fp64 trajectory on the same inputs and masks.  FR
+    evaluates one partition per group per step, N / c rows, which keeps the
+    host's fp64 run to about a minute."""
+    w = WORKLOADS["fr_logistic_n32_c4_d4096"]
+    _announce("%s full size, %d steps against the oracle's trajectory" % (w.name, w.steps))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    _check_trajectory(w, X, y, beta0, progress_every=10)
 
 
 EDGE = [
