@@ -219,6 +219,24 @@ def test_full_size_mlp_fresh_slots_match_the_oracle_at_every_iterate(full_mlp):
         sess.close()
 
 
+def test_full_size_mlp_trajectory_matches_oracle(full_mlp):
+    """All 1,048,576 rows and all 64 partitions: the decoded gradient and the
+    weights after every one of the workload's 20 steps against the oracle's
+    independent fp64 trajectory, within the bf16 bar."""
+    w, X, y, beta0 = full_mlp
+    _announce("%s full size, %d steps against the oracle's trajectory" % (w.name, w.steps))
+    masks_gpu, masks_or = gpu_masks(w), oracle_masks(w)
+    assert [m.tolist() for m in masks_gpu] == [m.tolist() for m in masks_or]
+    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu)
+    recs_or = oracle_run(w, *_host_inputs(X, y, beta0), masks_or, progress_every=2)
+    worst = 0.0
+    for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
+        e_g, e_w = normwise_error(g["ghat"], o.ghat), normwise_error(g["w"], o.beta)
+        worst = max(worst, e_g, e_w)
+        assert e_g <= BF16_TOL and e_w <= BF16_TOL, "step %d: %.3g %.3g" % (t, e_g, e_w)
+    print("  worst normwise error over %d steps: %.3g" % (w.steps, worst), flush=True)
+
+
 def test_full_size_mlp_runs_are_bitwise_reproducible(full_mlp):
     w, X, y, beta0 = full_mlp
     _announce("%s full size, run twice" % w.name)

@@ -5,9 +5,9 @@ from each side's own generator and must agree bit for bit; then the decoded
 gradient and the weights are compared after every step of independent
 trajectories (no re-syncing), normwise within 1e-5.
 
-Sizes: the small workloads run whole; the two large ones run their full
-trajectories with fewer rows per partition (same n, c, d, kernel shape).  At
-full size (the d = 1024, 4096 and 8192 workloads with all of their rows) every
+Sizes: every workload's whole trajectory runs at full size against the
+oracle's independent trajectory (the two largest also with fewer rows per
+partition, same n, c, d and kernel shape).  At full size, in addition, every
 ring copy of sampled partitions written at each of c + 2 steps is compared
 with the oracle's gradient at the iterate that step started from (the oracle
 fed the GPU's iterate), and properties that hold at any size are checked:
@@ -97,6 +97,37 @@ def test_full_size_fr_d4096_trajectory_matches_oracle():
     _announce("%s full size, %d steps against the oracle's trajectory" % (w.name, w.steps))
     X, y, beta0 = make_inputs(w, device="cuda")
     _check_trajectory(w, X, y, beta0, progress_every=10)
+
+
+def test_full_size_cr_d8192_trajectory_matches_oracle():
+    """The largest workload with all 2,097,152 rows (64 GiB of features): the
+    GPU's decoded gradient and weights after every one of its 30 steps against
+    the oracle's independent fp64 trajectory.  The host holds the features once,
+    widened to fp64 chunk by chunk (128 GiB)."""
+    w = WORKLOADS["cr_logistic_n128_c8_d8192"]
+    _announce("%s full size, %d steps against the oracle's trajectory" % (w.name, w.steps))
+    X, y, beta0 = make_inputs(w, device="cuda")
+    masks_gpu, masks_or = gpu_masks(w), oracle_masks(w)
+    assert [m.tolist() for m in masks_gpu] == [m.tolist() for m in masks_or]
+    recs_gpu, _ = gpu_run(w, X, y, beta0, masks_gpu)
+    yh, bh = _to_host(y, beta0)
+    Xh = np.empty((w.N, w.d), dtype=np.float64)
+    chunk = 1 << 16
+    for r in range(0, w.N, chunk):
+        Xh[r:r + chunk] = X[r:r + chunk].cpu().numpy()      # fp32 -> fp64 is exact
+        if (r + chunk) % (1 << 19) == 0:
+            print("  host copy: %d of %d rows" % (r + chunk, w.N), flush=True)
+    del X
+    torch.cuda.empty_cache()
+    recs_or = oracle_run(w, Xh, yh, bh, masks_or, progress_every=5)
+    del Xh
+    worst = 0.0
+    for t, (g, o) in enumerate(zip(recs_gpu, recs_or)):
+        e_g, e_w = normwise_error(g["ghat"], o.ghat), normwise_error(g["w"], o.beta)
+        worst = max(worst, e_g, e_w)
+        assert e_g <= FP32_TOL, "step %d: decoded gradient error %.3g" % (t, e_g)
+        assert e_w <= FP32_TOL, "step %d: weight error %.3g" % (t, e_w)
+    print("  worst normwise error over %d steps: %.3g" % (w.steps, worst), flush=True)
 
 
 EDGE = [
