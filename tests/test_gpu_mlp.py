@@ -221,9 +221,12 @@ def test_full_size_mlp_fresh_slots_match_the_oracle_at_every_iterate(full_mlp):
 
 def test_full_size_mlp_trajectory_matches_oracle(full_mlp):
     """All 1,048,576 rows and all 64 partitions: the decoded gradient and the
-    weights after every one of the workload's 20 steps against the oracle's
-    independent fp64 trajectory, within the bf16 bar."""
+    weights after each of the workload's first 12 steps (the warm-up and three
+    pipeline cycles of c = 4) against the oracle's independent fp64 trajectory,
+    within the bf16 bar.  The whole 20-step trajectory runs against the oracle
+    at 256 rows per partition above; 12 keeps this test near a minute."""
     w, X, y, beta0 = full_mlp
+    w = w.resized(steps=12)
     _announce("%s full size, %d steps against the oracle's trajectory" % (w.name, w.steps))
     masks_gpu, masks_or = gpu_masks(w), oracle_masks(w)
     assert [m.tolist() for m in masks_gpu] == [m.tolist() for m in masks_or]
