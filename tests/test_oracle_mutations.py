@@ -87,7 +87,8 @@ def _decode_step_ascent(*args, **kw):
 MUTANTS = {
     "slot index": ("coded_terms", _coded_terms_slot_off_by_one, [
         (pins.test_copies_are_at_most_c_minus_1_steps_stale, (O.CR, 7, 3)),
-        (pins.test_coded_gradients_equal_per_worker_rings, (O.CR, O.LSQ, 5, 3))]),
+        (pins.test_coded_gradients_equal_per_worker_rings, (O.CR, O.LSQ, 5, 3)),
+        (pins.test_naive_cr_matches_the_printed_n4_c2_example, ())]),
     "staleness": ("coded_terms", _coded_terms_no_staleness, [
         (pins.test_copies_are_at_most_c_minus_1_steps_stale, (O.FR, 8, 4)),
         (pins.test_cr_full_sum_identity_eq1, (5, 2))]),
@@ -98,10 +99,12 @@ MUTANTS = {
         (pins.test_fr_decode_picks_one_per_group_and_ignores_which, (6, 3)),
         (pins.test_decoder_rejects_too_many_stragglers, ())]),
     "placement": ("placement", _placement_reversed_cycle, [
-        (pins.test_cr_every_partition_has_c_holders, (O.CR, 7, 3))]),
+        (pins.test_cr_every_partition_has_c_holders, (O.CR, 7, 3)),
+        (pins.test_naive_cr_matches_the_printed_n4_c2_example, ())]),
     "transposed B": ("encoding_coefficients", _encoding_transposed, [
         (pins.test_real_code_decodes_exactly_for_every_admissible_set, (5, 2)),
-        (pins.test_real_code_decodes_exactly_for_every_admissible_set, (8, 3))]),
+        (pins.test_real_code_decodes_exactly_for_every_admissible_set, (8, 3)),
+        (pins.test_naive_cr_matches_the_printed_n4_c2_example, ())]),
     "1/m": ("partition_gradient", _gradient_sum_not_mean, [
         (pins.test_linear_gradients_match_finite_differences, (O.LSQ,)),
         (pins.test_c1_is_full_batch_gradient_descent, (O.CR, O.LSQ))]),

@@ -555,3 +555,41 @@ def test_elementwise_error_with_floor():
     assert elementwise_error(b * (1 + 1e-6), b) == pytest.approx(1e-6)
     # An absolute error of 1e-6 on the tiny entry is measured against 1e-3 * 10.
     assert elementwise_error(b + np.array([0.0, 1e-6, 0.0]), b) == pytest.approx(1e-4)
+
+
+def test_naive_cr_matches_the_printed_n4_c2_example():
+    """Sec. V-A's worked example of naive PGC-CR (n = 4, c = 2): D_1 decoded as
+    -g_1^(t-1) + 2 g_1^(t), the fresh copy from W_0's second slot, the stale one
+    from W_1's first (tests/golden/naive_cr_example_n4_c2.txt).  The example's
+    matrix is not printed; in the family of real codes used here (rows in the
+    null space of H, whose entries sum to zero), H = [-2, 1, a, 1 - a] with W_3
+    straggling yields exactly these coefficients for any a."""
+    with open(os.path.join(GOLDEN, "naive_cr_example_n4_c2.txt")) as f:
+        lines = [l.split() for l in f if l.strip() and not l.startswith("#")]
+    k = int(lines[0][1])
+    copies = [tuple(int(v) for v in l[1:]) for l in lines[1:]]
+    n, c = 4, 2
+    for a in (0.5, 0.3, -1.7):
+        H = np.array([[-2.0, 1.0, a, 1.0 - a]])
+        B = O.cyclic_encoding_matrix(n, c, H)
+        mask = np.array([0, 0, 0, 1], np.uint8)
+        J = O.survivors(mask)
+        d, scale = O.decode_weights(O.CR_REAL, n, c, J, B)
+        alpha = O.decoding_coefficients(O.CR_REAL, n, c, J, d, B)
+        P = O.placement(O.CR_REAL, n, c)
+        got = {}
+        for m, j in enumerate(J):
+            for l in range(c):
+                if P[j][l] == k:
+                    got[(j, l)] = n * scale * alpha[m, k]
+        assert sorted(got) == sorted((w, s) for w, s, _, _ in copies)
+        for w, s, _, coef in copies:
+            assert got[(w, s)] == pytest.approx(coef, abs=1e-12)
+        assert sum(got.values()) == pytest.approx(1.0, abs=1e-12)       # the coefficients sum to 1
+        # At a step t that evaluates the second slot, W_0's copy of D_1 is fresh
+        # and W_1's was evaluated at t - 1 (Sec. IV-A schedule, (t - 1) mod c).
+        for t in (2, 4, 6):
+            assert O.evaluated_slot(t, c) == 1
+            for w, s, offset, _ in copies:
+                terms = {slot: (part, tau) for slot, part, tau in O.coded_terms(O.CR_REAL, n, c, w, t)}
+                assert terms[s] == (k, t + offset)
