@@ -167,25 +167,37 @@ T* ws_ptr(const pgc_ctx* ctx, size_t off) {
 // Resolve recorded kernel events whose work has completed, or all of them.
 int resolve_timing(pgc_ctx* ctx, bool wait) {
   size_t done = 0;
+  int status = PGC_OK;
   for (; done < ctx->pending.size(); ++done) {
     Timed& tm = ctx->pending[done];
     if (wait) {
       hipError_t e = hipEventSynchronize(tm.stop);
-      if (e != hipSuccess) return device_fail(ctx, e, "hipEventSynchronize");
+      if (e != hipSuccess) {
+        status = device_fail(ctx, e, "hipEventSynchronize");
+        break;
+      }
     } else {
       const hipError_t q = hipEventQuery(tm.stop);
       if (q == hipErrorNotReady) break;
-      if (q != hipSuccess) return device_fail(ctx, q, "hipEventQuery");
+      if (q != hipSuccess) {
+        status = device_fail(ctx, q, "hipEventQuery");
+        break;
+      }
     }
     float ms = 0.f;
     hipError_t e = hipEventElapsedTime(&ms, tm.start, tm.stop);
-    if (e != hipSuccess) return device_fail(ctx, e, "hipEventElapsedTime");
+    if (e != hipSuccess) {
+      status = device_fail(ctx, e, "hipEventElapsedTime");
+      break;
+    }
     ctx->total_ms[tm.kernel] += ms;
     ctx->launches[tm.kernel] += 1;
     ctx->spare.push_back(tm);
   }
+  // Pairs already counted leave the pending list even when a later one fails,
+  // so no launch is counted twice and no pair is both pending and spare.
   ctx->pending.erase(ctx->pending.begin(), ctx->pending.begin() + done);
-  return PGC_OK;
+  return status;
 }
 
 // Launch `fn` on the context stream, bracketed by events when timing is on.

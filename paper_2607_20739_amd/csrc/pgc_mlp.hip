@@ -71,26 +71,34 @@ void mlp_cast_w2_kernel(MlpCastArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// forward: H = relu(X W1 + b1).  Block tile 256 rows x 256 hidden, K step 64,
-// 8 waves as 2 (rows) x 4 (hidden), 128 x 64 each, one block per CU.  Tiles
-// travel from global memory straight into LDS (16 bytes per lane, no register
-// staging) through two buffers, loaded one K step ahead: one barrier per K
-// step.  In a tile row of 64 bf16 (eight 16-byte chunks) chunk ch of row r
-// sits at slot ch ^ ((r ^ (r >> 3)) & 7), so the 16 rows of a fragment read
-// spread over the slots.  The MFMAs produce H^T (A = W1^T rows, B = X rows),
-// which leaves four consecutive hidden units of one sample in each lane.
-// Block ids are mapped so that all hidden tiles of a row tile run on the same
-// XCD (workgroups are dealt to the 8 XCDs round-robin) and share its L2.
+// forward: H = relu(X W1 + b1).  Block tile BM samples x 256 hidden, K step
+// 64, 8 waves as WH (hidden) x WS (samples), one block per CU.  With BM = 384
+// the waves are 2 x 4 of 128 hidden x 96 samples (192 fp32 accumulators per
+// lane) and a K step's two tiles fill the 160 KiB of LDS in two buffers: per
+// MFMA FLOP a quarter fewer fragment reads and a sixth fewer tile bytes than a
+// 256 x 256 tile, and a third fewer blocks to start and drain.  Tiles travel
+// from global memory straight into LDS (16 bytes per lane, no register
+// staging), loaded one K step ahead: one barrier per K step.  In a tile row of
+// 64 bf16 (eight 16-byte chunks) chunk ch of row r sits at slot
+// ch ^ (r & 7) ^ ((r >> 3) & 1), so the 16 rows of a fragment read spread over
+// the slots.  The MFMAs produce H^T (A = W1^T rows, B = X rows), which leaves four
+// consecutive hidden units of one sample in each lane.  Block ids are mapped
+// so that all hidden tiles of a row tile run on the same XCD (workgroups are
+// dealt to the 8 XCDs round-robin) and share its L2.
 // ---------------------------------------------------------------------------
 
-constexpr int kFwBM = 256, kFwBN = 256, kFwBK = 64, kFwStages = 2;
-static_assert(kFwBK == 32 || kFwBK == 64, "swizzle");
+constexpr int kFwBN = 256, kFwBK = 64, kFwStages = 2;
 constexpr int kFwThreads = 512;
-constexpr int kFwTile = kFwBM * kFwBK;          // bf16 per operand tile (32 KiB)
-constexpr int kFwRounds = kFwTile / 8 / kFwThreads;   // 16-byte chunks per thread per tile
+constexpr int kFwCpr = kFwBK / 8;                   // 16-byte chunks per tile row
+constexpr int kFwLdsBytes = 160 * 1024;
 constexpr int kXcds = 8;
-static_assert(kFwBM == kFwBN, "one load pattern serves both operand tiles");
-static_assert(kFwStages * 2 * kFwTile >= kFwBM * kFwBN, "the output tile is staged in the operand buffers");
+
+// Wave grid (hidden x samples) and epilogue passes per block tile height.
+// 256 x 256 tiles (4 x 2 waves of 64 x 128, one epilogue pass) measured 7%
+// slower than 384 x 256 on the 784 -> 1024 workload, with bitwise the same H.
+template <int BM> struct FwShape;
+template <> struct FwShape<384> { static constexpr int WH = 2, WS = 4, PASSES = 2; };
+constexpr int kFwBM = 384;   // samples per block tile
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
@@ -100,12 +108,16 @@ __device__ __forceinline__ void load_lds16(const void* src, void* lds_wave_base)
   __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)lds_wave_base, 16, 0, 0);
 }
 
-// Swizzle of a tile row's 16-byte chunks (an involution on 0 .. BK/8 - 1).
-__device__ __forceinline__ int fw_swizzle(int row) {
-  if constexpr (kFwBK == 32) return ((row >> 1) ^ (row >> 2)) & 3;
-  else return (row ^ (row >> 3)) & 7;
+// Swizzle of a tile row's 16-byte chunks: chunk ch of row r sits at slot
+// ch ^ fw_swizzle(r).  It depends only on the row within its 16-row group, so a
+// lane's fragment reads for successive 16-row groups are a constant stride
+// apart, and rows r and r + 8 of a group land in different slots.
+__device__ __forceinline__ int fw_swizzle(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+// 16 bytes from a wave-uniform base plus a per-lane byte offset to LDS.
+__device__ __forceinline__ void load_lds16_at(const bf16* base, uint32_t offset_bytes, void* lds_wave_base) {
+  load_lds16(reinterpret_cast<const char*>(base) + offset_bytes, lds_wave_base);
 }
-__device__ __forceinline__ int fw_slot(int row, int ch) { return row * kFwBK + ((ch ^ fw_swizzle(row)) << 3); }
 
 // Workgroup barrier that orders LDS only: the wave's own LDS reads and writes
 // complete (lgkmcnt 0) before it, but outstanding global loads and stores do
@@ -127,15 +139,28 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | n);
 }
 
+template <int BM>
 __global__ __launch_bounds__(kFwThreads, 1)
 void mlp_forward_kernel(MlpForwardArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16 smem[kFwStages][2][kFwTile];   // [buffer][X, W1^T]
+  using S = FwShape<BM>;
+  constexpr int kTH = kFwBN / S::WH, kTS = BM / S::WS;   // wave tile: hidden x samples
+  constexpr int kNT = kTH / 16, kMT = kTS / 16;
+  constexpr int kXTile = BM * kFwBK, kWTile = kFwBN * kFwBK;   // bf16 per operand tile
+  constexpr int kStage = kXTile + kWTile;
+  constexpr int kXRounds = kXTile / 8 / kFwThreads, kWRounds = kWTile / 8 / kFwThreads;
+  constexpr int kPassRows = BM / S::PASSES;   // output rows staged through LDS at a time
+  static_assert(S::WH * S::WS * 64 == kFwThreads && kTH % 16 == 0 && kTS % 16 == 0, "wave grid");
+  static_assert(kFwStages == 2, "one K step in flight: every load is waited for at the next barrier");
+  static_assert(kFwStages * kStage * 2 <= kFwLdsBytes, "LDS");
+  static_assert(kPassRows * kFwBN * 2 <= kFwStages * kStage * 2 && kPassRows % 16 == 0, "output staging");
+  static_assert(S::WS % S::PASSES == 0, "each pass stages whole sample groups");
+  __shared__ __attribute__((aligned(16))) bf16 smem[kFwStages * kStage];   // per buffer: X tile, W1^T tile
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int wr = wave >> 2, wh = wave & 3;
+  const int wh = wave % S::WH, ws = wave / S::WH;
 
   const int htiles = a.hidden / kFwBN;
-  const int64_t tiles_per_part = (a.m + kFwBM - 1) / kFwBM;
+  const int64_t tiles_per_part = (a.m + BM - 1) / BM;
   const int64_t rtiles = tiles_per_part * a.n_eval;
   const int64_t id = blockIdx.x;
   const int64_t rest = id / kXcds;
@@ -143,121 +168,126 @@ void mlp_forward_kernel(MlpForwardArgs a) {
   const int64_t rt = (rest / htiles) * kXcds + id % kXcds;
   if (rt >= rtiles) return;
   const int e = static_cast<int>(rt / tiles_per_part);
-  const int64_t r0 = (rt % tiles_per_part) * kFwBM;
+  const int64_t r0 = (rt % tiles_per_part) * BM;
   const int h0 = ht * kFwBN;
   const int64_t part = static_cast<int64_t>(e) * a.part_stride + a.part_offset;
   const bf16* Xp = a.X + part * a.m * a.d_in;
   const int ksteps = a.kpad / kFwBK;
   const int dchunks = a.d_in / 8;
-  constexpr int kCpr = kFwBK / 8;   // 16-byte chunks per tile row
 
-  // Chunk c = u * 512 + tid of a tile is row c / kCpr at slot c % kCpr, which
-  // holds the logical chunk given by the swizzle (an involution).  Rows past the partition read its last
+  // Chunk c = u * 512 + tid of a tile is row c / 8 = u * 64 + tid / 8 at slot
+  // c % 8 = tid % 8, which holds logical chunk (tid % 8) ^ swizzle(row); the
+  // swizzle does not change when 64 is added to the row, so the chunk is the
+  // same in every round.  Addresses are 32-bit byte offsets from the tile's
+  // first row (wave-uniform bases).  Rows past the partition read its last
   // row, chunks past d_in read the row's first chunk: both are finite values
   // that meet zero weights or land in rows that are never stored.
-  int64_t xoff[kFwRounds];
-  int32_t woff[kFwRounds], chunk[kFwRounds];
+  const int chunk = (tid & 7) ^ fw_swizzle(tid >> 3);
+  const bf16* Xt = Xp + r0 * a.d_in;
+  const int last_row = static_cast<int>(min<int64_t>(BM, a.m - r0)) - 1;
+  uint32_t xrow[kXRounds];
 #pragma unroll
-  for (int u = 0; u < kFwRounds; ++u) {
-    const int c = u * kFwThreads + tid, row = c / kCpr;
-    chunk[u] = (c % kCpr) ^ fw_swizzle(row);
-    xoff[u] = static_cast<int64_t>(r0 + row < a.m ? r0 + row : a.m - 1) * a.d_in;
-    woff[u] = (h0 + row) * a.kpad;
-  }
+  for (int u = 0; u < kXRounds; ++u)
+    xrow[u] = static_cast<uint32_t>(min(u * 64 + (tid >> 3), last_row)) * static_cast<uint32_t>(a.d_in) * 2u;
+  const bf16* Wt = a.W1T + static_cast<int64_t>(h0) * a.kpad;
+  const uint32_t wrow = static_cast<uint32_t>(tid >> 3) * static_cast<uint32_t>(a.kpad) * 2u;
   auto issue = [&](int ks, int buf) {
+    const int kc = ks * kFwCpr + chunk;
+    const uint32_t xk = static_cast<uint32_t>(kc < dchunks ? kc : 0) * 16u;
 #pragma unroll
-    for (int u = 0; u < kFwRounds; ++u) {
-      const int kc = ks * kCpr + chunk[u];
-      const int dst = (u * kFwThreads + wave * 64) * 8;
-      load_lds16(Xp + xoff[u] + (kc < dchunks ? kc * 8 : 0), &smem[buf][0][dst]);
-      load_lds16(a.W1T + woff[u] + kc * 8, &smem[buf][1][dst]);
-    }
+    for (int u = 0; u < kXRounds; ++u)
+      load_lds16_at(Xt, xrow[u] + xk, &smem[buf * kStage + (u * kFwThreads + wave * 64) * 8]);
+#pragma unroll
+    for (int u = 0; u < kWRounds; ++u)
+      load_lds16_at(Wt + static_cast<int64_t>(u * 64) * a.kpad, wrow + static_cast<uint32_t>(kc) * 16u,
+                    &smem[buf * kStage + kXTile + (u * kFwThreads + wave * 64) * 8]);
   };
 
-  f32x4 acc[4][8];   // [hidden tile][sample tile], D = H^T
+  f32x4 acc[kNT][kMT];   // [hidden tile][sample tile], D = H^T
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
+  for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) acc[nt][mt] = f32x4{};
+    for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = f32x4{};
+  // A lane reads rows ws * kTS + mt * 16 + lr of the X tile and
+  // wh * kTH + nt * 16 + lr of the W1^T tile, chunk kk * 4 + lg of each.
+  const int lane_swz = fw_swizzle(lr);
   auto compute = [&](int buf) {
-    const bf16* Xs = smem[buf][0];
-    const bf16* Ws = smem[buf][1];
+    const bf16* Xs = smem + buf * kStage + (ws * kTS + lr) * kFwBK;
+    const bf16* Ws = smem + buf * kStage + kXTile + (wh * kTH + lr) * kFwBK;
 #pragma unroll
     for (int kk = 0; kk < kFwBK / 32; ++kk) {
-      const int ch = kk * 4 + lg;
-      bf16x8 wf[4], xf[8];
+      const int slot = ((kk * 4 + lg) ^ lane_swz) << 3;
+      bf16x8 xf[kMT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-        wf[nt] = *reinterpret_cast<const bf16x8*>(&Ws[fw_slot(wh * 64 + nt * 16 + lr, ch)]);
+      for (int mt = 0; mt < kMT; ++mt) xf[mt] = *reinterpret_cast<const bf16x8*>(Xs + mt * 16 * kFwBK + slot);
 #pragma unroll
-      for (int mt = 0; mt < 8; ++mt)
-        xf[mt] = *reinterpret_cast<const bf16x8*>(&Xs[fw_slot(wr * 128 + mt * 16 + lr, ch)]);
+      for (int nt = 0; nt < kNT; ++nt) {
+        const bf16x8 wf = *reinterpret_cast<const bf16x8*>(Ws + nt * 16 * kFwBK + slot);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) acc[nt][mt] = mfma_k32(wf[nt], xf[mt], acc[nt][mt]);
+        for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = mfma_k32(wf, xf[mt], acc[nt][mt]);
+      }
     }
   };
 
-  // Each issue() is 2 * kFwRounds loads per lane.  At the top of step ks the
-  // steps after ks already issued are min(kFwStages - 2, ksteps - 1 - ks).
-  constexpr int kLoads = 2 * kFwRounds;
-  static_assert(kFwStages >= 2 && kFwStages <= 4 && (kFwStages - 2) * kLoads < 16, "vmcnt field");
-#pragma unroll
-  for (int p = 0; p < kFwStages - 1; ++p)
-    if (p < ksteps) issue(p, p);
+  issue(0, 0);
   for (int ks = 0; ks < ksteps; ++ks) {
     // This wave's loads of step ks have landed; after the barrier every
-    // wave's have, and every wave is done reading buffer (ks - 1) % kFwStages,
-    // which the loads of step ks + kFwStages - 1 then overwrite.
-    const int later = min(kFwStages - 2, ksteps - 1 - ks);
-    if (later >= 2) wait_vmcnt<(kFwStages >= 4 ? 2 * kLoads : 0)>();
-    else if (later == 1) wait_vmcnt<(kFwStages >= 3 ? kLoads : 0)>();
-    else wait_vmcnt<0>();
+    // wave's have, and every wave is done reading buffer (ks + 1) % 2, which
+    // the loads of step ks + 1 then overwrite.
+    wait_vmcnt<0>();
     lds_barrier();
-    if (ks + kFwStages - 1 < ksteps) issue(ks + kFwStages - 1, (ks + kFwStages - 1) % kFwStages);
+    if (ks + 1 < ksteps) issue(ks + 1, (ks + 1) % kFwStages);
     compute(ks % kFwStages);
   }
 
-  // Epilogue: bias and ReLU, then the 256 x 256 bf16 tile goes through LDS
-  // (row r's 16-byte chunk cc at slot cc ^ (r & 31)) so that H leaves in its
-  // blocked layout, 1 KiB of contiguous memory per store instruction.
+  // Epilogue: bias and ReLU, then the tile goes through LDS, kPassRows rows at
+  // a time (row r's 16-byte chunk cc at slot cc ^ (r & 31)), so that H leaves
+  // in its blocked layout, 1 KiB of contiguous memory per store instruction.
   lds_barrier();   // every wave is done reading the operand buffers
-  bf16* out = &smem[0][0][0];
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    const int hl = wh * 64 + nt * 16 + lg * 4;   // hidden column within the tile
-    float bias[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) bias[i] = a.b1[h0 + hl + i];
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt) {
-      const int r = wr * 128 + mt * 16 + lr;
-      bf16x4 v;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = static_cast<bf16>(fmaxf(acc[nt][mt][i] + bias[i], 0.0f));
-      *reinterpret_cast<bf16x4*>(&out[r * kFwBN + (((hl >> 3) ^ (r & 31)) << 3) + (hl & 4)]) = v;
-    }
-  }
-  lds_barrier();
-  // The tile is 16 row blocks x 2 hidden blocks of 4 KiB; chunk q of a block
-  // is fragment slice q / 64, lane q % 64 (row q % 16, 8-unit group (q / 16) % 4).
+  bf16* out = smem;
   const int64_t hblocks = a.hidden / 128;
   bf16* Hb = a.H + ((static_cast<int64_t>(e) * (a.m_pad / 16) + r0 / 16) * hblocks + h0 / 128) * 2048;
-#pragma unroll 4
-  for (int it = 0; it < kFwBM * kFwBN / 8 / kFwThreads; ++it) {
-    const int q = it * kFwThreads + tid;
-    const int blk = q >> 8, rbl = blk >> 1, hbl = blk & 1, within = q & 255;
-    const int r = rbl * 16 + (within & 15);
-    const int cc = hbl * 16 + (within >> 6) * 4 + ((within >> 4) & 3);
-    const int64_t row = r0 + r;
-    if (row < a.m_pad) {
-      const bf16x8 v = row < a.m ? *reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)])
-                                 : bf16x8{};
-      // H (2 GB per step) cannot stay in the caches until the head reads it:
-      // streaming stores keep it from evicting the reused X and W1^T tiles.
-      __builtin_nontemporal_store(v, reinterpret_cast<bf16x8*>(Hb + (rbl * hblocks + hbl) * 2048 + within * 8));
+  constexpr int kGroupsPerPass = S::WS / S::PASSES;
+#pragma unroll
+  for (int p = 0; p < S::PASSES; ++p) {
+    if (ws / kGroupsPerPass == p) {
+#pragma unroll
+      for (int nt = 0; nt < kNT; ++nt) {
+        const int hl = wh * kTH + nt * 16 + lg * 4;   // hidden column within the tile
+        float bias[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bias[i] = a.b1[h0 + hl + i];
+#pragma unroll
+        for (int mt = 0; mt < kMT; ++mt) {
+          const int r = (ws % kGroupsPerPass) * kTS + mt * 16 + lr;   // row within the pass
+          bf16x4 v;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = static_cast<bf16>(fmaxf(acc[nt][mt][i] + bias[i], 0.0f));
+          *reinterpret_cast<bf16x4*>(&out[r * kFwBN + (((hl >> 3) ^ (r & 31)) << 3) + (hl & 4)]) = v;
+        }
+      }
     }
+    lds_barrier();
+    // The pass is kPassRows / 16 row blocks x 2 hidden blocks of 4 KiB; chunk
+    // q of a block is fragment slice q / 64, lane q % 64 (row q % 16, 8-unit
+    // group (q / 16) % 4).
+#pragma unroll 4
+    for (int it = 0; it < kPassRows * kFwBN / 8 / kFwThreads; ++it) {
+      const int q = it * kFwThreads + tid;
+      const int blk = q >> 8, rbl = blk >> 1, hbl = blk & 1, within = q & 255;
+      const int r = rbl * 16 + (within & 15);
+      const int cc = hbl * 16 + (within >> 6) * 4 + ((within >> 4) & 3);
+      const int64_t row = r0 + p * kPassRows + r;
+      if (row < a.m_pad) {
+        const bf16x8 v = row < a.m ? *reinterpret_cast<const bf16x8*>(&out[r * kFwBN + ((cc ^ (r & 31)) << 3)])
+                                   : bf16x8{};
+        // H (2 GB per step) cannot stay in the caches until the head reads it:
+        // streaming stores keep it from evicting the reused X and W1^T tiles.
+        __builtin_nontemporal_store(
+            v, reinterpret_cast<bf16x8*>(Hb + ((p * kPassRows / 16 + rbl) * hblocks + hbl) * 2048 + within * 8));
+      }
+    }
+    if (p + 1 < S::PASSES) lds_barrier();   // the next pass overwrites the staging area
   }
 }
 
@@ -664,7 +694,7 @@ hipError_t launch_mlp_cast(const MlpCastArgs& a, hipStream_t s) {
 hipError_t launch_mlp_forward(const MlpForwardArgs& a, hipStream_t s) {
   const int64_t rtiles = (a.m + kFwBM - 1) / kFwBM * a.n_eval;
   dim3 grid(static_cast<unsigned>((rtiles + kXcds - 1) / kXcds * kXcds * (a.hidden / kFwBN)));
-  hipLaunchKernelGGL(mlp_forward_kernel, grid, dim3(kFwThreads), 0, s, a);
+  hipLaunchKernelGGL(mlp_forward_kernel<kFwBM>, grid, dim3(kFwThreads), 0, s, a);
   return hipGetLastError();
 }
 
