@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "pgc_kernels.h"
 #include "pgc_lanes.h"
@@ -191,8 +192,14 @@ void mlp_forward_kernel(MlpForwardArgs a) {
     xrow[u] = static_cast<uint32_t>(min(u * 64 + (tid >> 3), last_row)) * static_cast<uint32_t>(a.d_in) * 2u;
   const bf16* Wt = a.W1T + static_cast<int64_t>(h0) * a.kpad;
   const uint32_t wrow = static_cast<uint32_t>(tid >> 3) * static_cast<uint32_t>(a.kpad) * 2u;
-  auto issue = [&](int ks, int buf) {
+  // The last K step covers columns kpad - 64 .. kpad - 1.  When its second
+  // half lies wholly past d_in (784 features: 800 .. 831), that half is
+  // neither loaded nor multiplied: its products with the zero W1^T columns
+  // are exact zeros.
+  const bool half_last = a.kpad - 32 >= a.d_in;
+  auto issue = [&](int ks, int buf, bool skip_upper) {
     const int kc = ks * kFwCpr + chunk;
+    if (skip_upper && chunk >= kFwCpr / 2) return;
     const uint32_t xk = static_cast<uint32_t>(kc < dchunks ? kc : 0) * 16u;
 #pragma unroll
     for (int u = 0; u < kXRounds; ++u)
@@ -211,11 +218,12 @@ void mlp_forward_kernel(MlpForwardArgs a) {
   // A lane reads rows ws * kTS + mt * 16 + lr of the X tile and
   // wh * kTH + nt * 16 + lr of the W1^T tile, chunk kk * 4 + lg of each.
   const int lane_swz = fw_swizzle(lr);
-  auto compute = [&](int buf) {
+  // MFMAs over 32-column halves [K0, K1) of the K step held in buffer buf.
+  auto compute = [&](int buf, auto k0, auto k1) {
     const bf16* Xs = smem + buf * kStage + (ws * kTS + lr) * kFwBK;
     const bf16* Ws = smem + buf * kStage + kXTile + (wh * kTH + lr) * kFwBK;
 #pragma unroll
-    for (int kk = 0; kk < kFwBK / 32; ++kk) {
+    for (int kk = decltype(k0)::value; kk < decltype(k1)::value; ++kk) {
       const int slot = ((kk * 4 + lg) ^ lane_swz) << 3;
       bf16x8 xf[kMT];
 #pragma unroll
@@ -229,16 +237,24 @@ void mlp_forward_kernel(MlpForwardArgs a) {
     }
   };
 
-  issue(0, 0);
-  for (int ks = 0; ks < ksteps; ++ks) {
+  using H0 = std::integral_constant<int, 0>;
+  using H1 = std::integral_constant<int, 1>;
+  using H2 = std::integral_constant<int, 2>;
+  static_assert(kFwBK == 64, "two 32-column halves per K step");
+  issue(0, 0, ksteps == 1 && half_last);
+  for (int ks = 0; ks + 1 < ksteps; ++ks) {
     // This wave's loads of step ks have landed; after the barrier every
     // wave's have, and every wave is done reading buffer (ks + 1) % 2, which
     // the loads of step ks + 1 then overwrite.
     wait_vmcnt<0>();
     lds_barrier();
-    if (ks + 1 < ksteps) issue(ks + 1, (ks + 1) % kFwStages);
-    compute(ks % kFwStages);
+    issue(ks + 1, (ks + 1) % kFwStages, ks + 2 == ksteps && half_last);
+    compute(ks % kFwStages, H0{}, H2{});
   }
+  wait_vmcnt<0>();
+  lds_barrier();
+  compute((ksteps - 1) % kFwStages, H0{}, H1{});
+  if (!half_last) compute((ksteps - 1) % kFwStages, H1{}, H2{});
 
   // Epilogue: bias and ReLU, then the tile goes through LDS, kPassRows rows at
   // a time (row r's 16-byte chunk cc at slot cc ^ (r & 31)), so that H leaves
