@@ -84,7 +84,9 @@ enum pgc_kernel {
 };
 
 #define PGC_MAX_N 256           /* largest number of workers */
-/* MLP shape limits: d_in % 8 == 0, hidden % 256 == 0, hidden <= 1024, 1 <= classes <= 16. */
+/* MLP shape limits: d_in % 8 == 0, d_in <= 2^20, hidden % 256 == 0, hidden <= 1024,
+ * 1 <= classes <= 16. */
+#define PGC_MLP_MAX_D_IN 1048576
 #define PGC_MLP_MAX_HIDDEN 1024
 #define PGC_MLP_MAX_CLASSES 16
 #define PGC_MAX_LINEAR_D 32768  /* largest feature count of the linear models (d % 4 == 0) */

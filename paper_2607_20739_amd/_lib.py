@@ -21,6 +21,7 @@ PGC_KERNEL_GRADIENT, PGC_KERNEL_REDUCE, PGC_KERNEL_CODE = 0, 1, 2
 PGC_KERNEL_MLP_CAST, PGC_KERNEL_MLP_FORWARD, PGC_KERNEL_MLP_HEAD, PGC_KERNEL_MLP_WGRAD = 3, 4, 5, 6
 PGC_MAX_N = 256
 PGC_NOALLOC_SCRATCH_BYTES = 32 << 20
+PGC_MLP_MAX_D_IN = 1 << 20
 
 SCHEMES = {"FR": PGC_FR, "CR": PGC_CR, "CR_REAL": PGC_CR_REAL, "IS_SGD": PGC_IS_SGD}
 MODELS = {"logistic": PGC_LOGISTIC, "lsq": PGC_LSQ, "mlp": PGC_MLP}

@@ -315,6 +315,8 @@ int pgc_configure(pgc_ctx* ctx, const pgc_config* cfg) {
   } else if (cfg->model == PGC_MLP) {
     const int64_t d_in = cfg->d_in, hidden = cfg->hidden, classes = cfg->classes;
     if (d_in < 8 || d_in % 8 != 0) return fail(ctx, PGC_EINVAL, "MLP d_in must be a positive multiple of 8");
+    // The forward GEMM addresses a row tile of X with 32-bit byte offsets.
+    if (d_in > PGC_MLP_MAX_D_IN) return fail(ctx, PGC_EINVAL, "MLP d_in exceeds PGC_MLP_MAX_D_IN");
     if (hidden < 256 || hidden % 256 != 0 || hidden > PGC_MLP_MAX_HIDDEN)
       return fail(ctx, PGC_EINVAL, "MLP hidden must be a multiple of 256 up to PGC_MLP_MAX_HIDDEN");
     if (classes < 1 || classes > PGC_MLP_MAX_CLASSES)

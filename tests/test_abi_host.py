@@ -160,6 +160,52 @@ def test_is_sgd_decode_ignores_any_number_of_stragglers():
         P.pgc_init("IS_SGD", 6, 2, 8)        # IS-SGD holds one partition per worker
 
 
+def test_binding_constants_match_header():
+    """Every numeric #define of include/pgc.h that the binding mirrors has the same value."""
+    with open(os.path.join(ROOT, "include", "pgc.h")) as f:
+        header = f.read()
+    defines = {}
+    for name, expr in re.findall(r"^#define (PGC_\w+)\s+(\(?[0-9u <]+\)?)", header, re.M):
+        parts = expr.strip("() ").replace("u", "").split("<<")   # "N" or "(Nu << K)"
+        defines[name] = int(parts[0]) << (int(parts[1]) if len(parts) > 1 else 0)
+    mirrored = [k for k in defines if hasattr(P, k)]
+    assert {"PGC_MAX_N", "PGC_NOALLOC_SCRATCH_BYTES", "PGC_MLP_MAX_D_IN"} <= set(mirrored)
+    for k in mirrored:
+        assert getattr(P, k) == defines[k], k
+
+
+def _mlp_d(d_in, hidden, classes):
+    return d_in * hidden + hidden + hidden * classes + classes
+
+
+def test_mlp_shape_limits():
+    """pgc_configure accepts the MLP shapes include/pgc.h allows and rejects the others."""
+    cases = [(64, 256, 10, True), (8, 1024, 16, True), (P.PGC_MLP_MAX_D_IN, 256, 10, True),
+             (P.PGC_MLP_MAX_D_IN + 8, 256, 10, False),   # past the forward's 32-bit tile offsets
+             (60, 256, 10, False), (0, 256, 10, False),   # d_in % 8, d_in >= 8
+             (64, 384, 10, False), (64, 2048, 10, False),  # hidden % 256, hidden <= 1024
+             (64, 256, 0, False), (64, 256, 17, False)]    # 1 <= classes <= 16
+    for d_in, hidden, classes, ok in cases:
+        ctx = P.pgc_init("CR", 4, 2, _mlp_d(d_in, hidden, classes))
+        try:
+            if ok:
+                P.pgc_configure(ctx, "mlp", 4 * 64, d_in, hidden, classes)
+                assert P.pgc_workspace_bytes(ctx) > 0
+            else:
+                with pytest.raises(P.PGCError) as e:
+                    P.pgc_configure(ctx, "mlp", 4 * 64, d_in, hidden, classes)
+                assert e.value.status == P.PGC_EINVAL, (d_in, hidden, classes)
+        finally:
+            P.pgc_destroy(ctx)
+    ctx = P.pgc_init("CR", 4, 2, _mlp_d(64, 256, 10) + 1)   # d must match the shape
+    try:
+        with pytest.raises(P.PGCError) as e:
+            P.pgc_configure(ctx, "mlp", 4 * 64, 64, 256, 10)
+        assert e.value.status == P.PGC_EINVAL
+    finally:
+        P.pgc_destroy(ctx)
+
+
 def test_error_codes():
     with pytest.raises(P.PGCError) as e:
         P.pgc_init("FR", 6, 4, 8)                      # c does not divide n
