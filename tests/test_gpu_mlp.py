@@ -68,13 +68,18 @@ SMALL = [
              policy=POLICY_UNIFORM_COUNT, cap=2, seed=33, hidden=512, classes=16),
     # several tiles of every kernel: d_in = 456 spans three 224-wide feature tiles of the
     # weight gradient (the last ragged), hidden = 768 three forward column tiles, m = 600
-    # three 256-row forward tiles (the last ragged)
+    # two 384-row forward tiles (the last ragged, with a partial second epilogue pass)
     Workload("mlp_cr_multi_tile", "CR", "mlp", n=4, c=2, N=4 * 600, d=456, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=35, hidden=768, classes=7),
     # five rows per partition: one ragged 16-row head tile, one 64-row weight-gradient K step,
     # and a forward tile that is almost all clamped rows
     Workload("mlp_cr_tiny_partitions", "CR", "mlp", n=4, c=2, N=4 * 5, d=16, lr=0.05, steps=5,
              policy=POLICY_EXACT, cap=1, seed=36, hidden=256, classes=4),
+    # m = 385: a second 384-row forward tile holding one row; d_in = 72 pads to two 64-column
+    # K steps whose last one skips its upper half (columns 96 .. 127 lie past d_in), and ends
+    # in a half-filled 16-feature block of the weight gradient
+    Workload("mlp_cr_forward_tile_edge", "CR", "mlp", n=4, c=2, N=4 * 385, d=72, lr=0.05, steps=5,
+             policy=POLICY_EXACT, cap=1, seed=38, hidden=256, classes=5),
     # the real-valued code on the MLP
     Workload("mlp_real_code", "CR_REAL", "mlp", n=4, c=2, N=4 * 64, d=64, lr=0.02, steps=5,
              policy=POLICY_EXACT, cap=1, seed=34, hidden=256, classes=10, code_seed=3),
