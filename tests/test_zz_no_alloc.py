@@ -1,9 +1,9 @@
 """pgc_step_noalloc (the step with its scratch in the library's fixed device
 array, for callers that cannot allocate) against pgc_step, through the C ABI.
 
-Two calls in a row on one GPU, the second with a smaller problem: the fixed
-array keeps the first call's contents, and the second must not depend on
-them.  The two entry points run the same kernels on the same grid, so the
+Calls in a row on one GPU, each with a smaller problem than the one before:
+the fixed array keeps the earlier call's contents, and a later call must not
+depend on them.  The two entry points run the same kernels on the same grid, so the
 decoded gradients and weights must agree bit for bit (well within the fp32
 bar of 1e-5).
 """
@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import paper_2607_20739_amd as P
-from workloads import Workload, make_inputs, POLICY_BERNOULLI, POLICY_UNIFORM_COUNT
+from workloads import Workload, make_inputs, POLICY_BERNOULLI, POLICY_EXACT, POLICY_UNIFORM_COUNT
 
 from _parity import FP32_TOL, gpu_masks, gpu_session, normwise_error
 
@@ -25,6 +25,9 @@ LARGE = Workload("noalloc_cr_logistic_d8192", "CR", "logistic", n=16, c=4, N=16 
                  lr=0.05, steps=7, policy=POLICY_BERNOULLI, cap=3, p=0.2, seed=71)
 SMALL = Workload("noalloc_real_lsq_d1000", "CR_REAL", "lsq", n=6, c=3, N=6 * 300, d=1000,
                  lr=0.02, steps=6, policy=POLICY_UNIFORM_COUNT, cap=2, seed=72, code_seed=4)
+# FR: every pipelined step evaluates one partition per group (a strided subset).
+TINY_FR = Workload("noalloc_fr_logistic_d64", "FR", "logistic", n=4, c=2, N=4 * 512, d=64,
+                   lr=0.1, steps=6, policy=POLICY_EXACT, cap=1, seed=73)
 
 
 def _announce(what):
@@ -50,14 +53,16 @@ def _run(w, noalloc):
 
 
 def test_noalloc_step_matches_pgc_step_on_two_calls_in_a_row():
-    sizes = {}
-    for w in (LARGE, SMALL):
+    problems = (LARGE, SMALL, TINY_FR)
+    sizes = []
+    for w in problems:
         sess = gpu_session(w)
         try:
-            sizes[w.name] = P.pgc_workspace_bytes(sess.ctx)
+            sizes.append(P.pgc_workspace_bytes(sess.ctx))
         finally:
             sess.close()
-    for w in (LARGE, SMALL):
+    assert sizes == sorted(sizes, reverse=True) and len(set(sizes)) == len(sizes), sizes   # each call smaller
+    for w in problems:
         _announce("%s n=%d c=%d d=%d N=%d" % (w.name, w.n, w.c, w.d, w.N))
         ref = _run(w, noalloc=False)
         got = _run(w, noalloc=True)
